@@ -1,0 +1,297 @@
+#!/usr/bin/env python3
+"""Throughput of the splice path on one MI355X.
+
+One step is one pass of the whole path over one batch of synthetic input already resident in
+HBM: splice the compiled block(s) into the paged cache (all layers), re-anchor their keys in
+place (all layers), splice the user-turn tokens, then run the suffix-redecode attention of every
+layer back to back.  Default workload: Qwen2.5-14B attention shapes, 48 layers, a 1024-token
+block spliced at depth 16384 with a full (R = 100%) redecode of the block plus 64 user tokens
+over a 17472-token cache.
+
+Prints one JSON line.  ``value`` is the whole-step attention throughput (algorithmic attention
+FLOPs per step / step time, TFLOP/s); ``roofline`` reports the attention kernel against the bf16
+MFMA peak and ``roofline_hbm`` the splice and re-anchor kernels against HBM bandwidth, all on
+algorithmic work.  ``cpu_baseline`` times the fp64 oracle on a bounded sample of
+the same workload on the host cores.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import subprocess
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+HBM_PEAK_GBPS = 8000.0           # MI355X HBM3E
+METRIC = "suffix-redecode attn TFLOP/s + re-phase/splice GB/s, % of MI355X roofline"
+
+
+def attn_flops(wl) -> float:
+    """4 D H_q sum_i (n_past + i + 1) per layer and block: QK^T and PV over unmasked pairs."""
+    tot = 0
+    for n_past in wl.attn_n_past:
+        n = wl.n_suffix
+        tot += 4 * wl.head_dim * wl.n_q_heads * (n * n_past + n * (n + 1) // 2)
+    return float(tot)
+
+
+def setup(cfg: int):
+    import torch
+    from paper_2608_20397_amd import nexus as N
+    from synth import PAGE
+    from synth import gen as G
+
+    wl = G.get_workload(cfg)
+    dev = "cuda"
+    L, H, D, Hq, T = wl.n_layers, wl.n_kv_heads, wl.head_dim, wl.n_q_heads, wl.block_len
+    nb = len(wl.splice_pos)
+    n_ctx = wl.n_tokens if nb > 1 else wl.splice_pos[0]
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+
+    def dn(tag, shape, std, off=0):
+        return torch.stack([G.device_normal(cfg, l, tag + off, shape, std, wl.dtype, dev)
+                            for l in range(L)])
+
+    TG = G.TAG
+    vl = N.V_TRANSPOSED if wl.v_layout == "transposed" else N.V_ROWMAJOR
+    npp = wl.n_pages
+    k = torch.zeros((L, npp, H, PAGE, D), dtype=dt, device=dev)
+    v = torch.zeros((L, H, D, npp * PAGE) if vl == N.V_TRANSPOSED else (L, npp, H, PAGE, D),
+                    dtype=dt, device=dev)
+    pm = torch.from_numpy(G.page_map(cfg, npp, wl.shuffled_pages)).to(dev)
+    cache = N.PagedKVCache(k, v, pm, wl.rope_base, vl)
+    ctx = N.Block(dn(TG["k_ctx"], (n_ctx, H, D), wl.k_scale), dn(TG["v_ctx"], (n_ctx, H, D), wl.v_scale),
+                  0, wl.rope_base)
+    N.splice_pages(cache, ctx, 0)                       # context: set-up, not timed
+    blocks = [N.Block(dn(TG["k_blk"], (T, H, D), wl.k_scale, 16 * b),
+                      dn(TG["v_blk"], (T, H, D), wl.v_scale, 16 * b), wl.anchor, wl.rope_base)
+              for b in range(nb)]
+    user = None
+    if wl.n_user:
+        u0 = wl.splice_pos[0] + T
+        user = (N.Block(dn(TG["k_user"], (wl.n_user, H, D), wl.k_scale),
+                        dn(TG["v_user"], (wl.n_user, H, D), wl.v_scale), u0, wl.rope_base), u0)
+    q = dn(TG["q"], (wl.n_suffix * nb, Hq, D), wl.q_scale)
+    out = torch.empty_like(q)
+    if nb == 1:
+        ws_bytes = N.suffix_attn_workspace_bytes(cache, wl.n_suffix, Hq, wl.attn_n_past[0])
+    else:
+        import ctypes as C
+        n = nb
+        ws_bytes = N.lib().nexus_suffix_attn_varlen_workspace(
+            n, (C.c_int32 * n)(*[b * wl.n_suffix for b in range(n)]),
+            (C.c_int32 * n)(*[wl.n_suffix] * n), (C.c_int64 * n)(*wl.attn_n_past), Hq,
+            C.byref(cache.c()))
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
+    del ctx
+    torch.cuda.synchronize()
+    return dict(wl=wl, cache=cache, blocks=blocks, user=user, q=q, out=out, ws=ws)
+
+
+def run_step(S, events=None):
+    """One pass of the path; ``events`` collects (kind, start, end) CUDA events per call."""
+    import torch
+    from paper_2608_20397_amd import nexus as N
+    wl, cache = S["wl"], S["cache"]
+
+    def timed(kind, fn):
+        if events is None:
+            fn()
+            return
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        events.append((kind, a, b))
+
+    for b, pos in enumerate(wl.splice_pos):
+        blk = S["blocks"][b]
+        timed("splice", lambda: N.splice_pages(cache, blk, pos))
+        timed("rephase", lambda: N.rephase_k_paged(cache, pos, wl.block_len, wl.anchor, pos,
+                                                   wl.rope_base))
+    if S["user"] is not None:
+        ub, u0 = S["user"]
+        timed("splice_user", lambda: N.splice_pages(cache, ub, u0))
+    nb = len(wl.splice_pos)
+    for layer in range(wl.n_layers):
+        if nb == 1:
+            timed("attn", lambda: N.suffix_attn(S["q"][layer], cache, layer, wl.attn_n_past[0],
+                                                wl.softcap, out=S["out"][layer],
+                                                workspace=S["ws"]))
+        else:
+            timed("attn", lambda: N.suffix_attn_varlen(
+                S["q"][layer], [b * wl.n_suffix for b in range(nb)], [wl.n_suffix] * nb,
+                list(wl.attn_n_past), cache, layer, wl.softcap, out=S["out"][layer],
+                workspace=S["ws"]))
+
+
+def cpu_baseline(cfg: int, n_kv_sample: int):
+    """The fp64 oracle on a bounded sample: one layer's splice + re-anchor (all heads) and the
+    attention of ``n_kv_sample`` KV heads' query groups, scaled to the whole step."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import oracle as O
+    from synth import PAGE
+    from synth import gen as G
+
+    wl = G.get_workload(cfg)
+    hc = G.host_case_wl(__import__("dataclasses").replace(wl, n_layers=1), cfg, layers=[0])
+    pm = hc.page_map
+    t0 = time.perf_counter()
+    ck, cv = G.empty_cache_bits(hc.wl, 1)
+    ck, cv = O.splice_paged(ck, cv, pm, hc.ctx_k, hc.ctx_v, 0, PAGE, wl.v_layout)
+    t_setup = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    for b, pos in enumerate(wl.splice_pos):
+        ck, cv = O.splice_paged(ck, cv, pm, hc.blk_k[b], hc.blk_v[b], pos, PAGE, wl.v_layout)
+        ck = O.rephase_paged_bits(ck, wl.dtype, pm, PAGE, pos, wl.block_len, wl.anchor, pos,
+                                  wl.rope_base)
+    if wl.n_user:
+        u0 = wl.splice_pos[0] + wl.block_len
+        ck, cv = O.splice_paged(ck, cv, pm, hc.user_k, hc.user_v, u0, PAGE, wl.v_layout)
+    t_splice = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    G_ = wl.group
+    n_keys = max(wl.attn_n_past) + wl.n_suffix
+    lk, lv = O.gather_logical(ck, cv, pm, n_keys, PAGE, wl.v_layout)
+    k = O.storage_to_f64(lk[0], wl.dtype)
+    v = O.storage_to_f64(lv[0], wl.dtype)
+    for b, n_past in enumerate(wl.attn_n_past):
+        qb = O.storage_to_f64(hc.q[0, b * wl.n_suffix:(b + 1) * wl.n_suffix], wl.dtype)
+        for g in range(n_kv_sample):
+            O.suffix_attention(qb[:, g * G_:(g + 1) * G_], k[:, g:g + 1], v[:, g:g + 1], n_past,
+                               softcap=wl.softcap)
+    t_attn = time.perf_counter() - t0
+    step_s = wl.n_layers * (t_splice + t_attn * wl.n_kv_heads / n_kv_sample)
+    flops = attn_flops(wl) * wl.n_layers
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {
+        "value": flops / step_s / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"layer 0 only: splice + re-anchor of all {wl.n_kv_heads} KV heads "
+                   f"({t_splice:.2f} s) and attention of {n_kv_sample} of {wl.n_kv_heads} KV-head "
+                   f"query groups ({t_attn:.2f} s), scaled x{wl.n_layers} layers and "
+                   f"x{wl.n_kv_heads / n_kv_sample:g} heads to one step; fp64 numpy, BLAS threads "
+                   f"for the matmuls, elementwise exp single-threaded"),
+        "step_s_estimate": step_s,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=3, choices=[2, 3, 4, 5])
+    ap.add_argument("--cpu-kv-sample", type=int, default=4,
+                    help="KV heads of layer 0 the oracle baseline computes (0 skips it)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only (no multi-GPU path); use --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_20397_amd import nexus as N
+    N.lib()   # fail loudly if the library is not built
+    torch.cuda.set_device(0)
+    S = setup(args.config)
+    wl = S["wl"]
+    print(f"bench: cfg{wl.cfg} {wl.name}: setup done", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        run_step(S)
+    torch.cuda.synchronize()
+    events = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        run_step(S, events)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / args.steps
+    dur = {}
+    for kind, a, b in events:
+        dur.setdefault(kind, []).append(a.elapsed_time(b))
+    mean = {k: sum(v) / len(v) for k, v in dur.items()}
+    print(f"bench: {args.steps} steps, {ms:.3f} ms/step, mean call ms {mean}", file=sys.stderr,
+          flush=True)
+
+    esize = 2 if wl.dtype == "bf16" else 4
+    nb = len(wl.splice_pos)
+    blk_bytes = wl.n_layers * wl.block_len * wl.n_kv_heads * wl.head_dim * esize   # K (or V) of one block
+    splice_bytes = 2 * 2 * blk_bytes          # read + write, K and V
+    rephase_bytes = 2 * blk_bytes             # read + write, K
+    fl_layer = attn_flops(wl)
+    step_flops = fl_layer * wl.n_layers
+    attn_tflops = fl_layer / (mean["attn"] * 1e-3) / 1e12
+    splice_gbps = splice_bytes / (mean["splice"] * 1e-3) / 1e9
+    rephase_gbps = rephase_bytes / (mean["rephase"] * 1e-3) / 1e9
+    rs_gbps = (splice_bytes + rephase_bytes) / ((mean["splice"] + mean["rephase"]) * 1e-3) / 1e9
+
+    res = {
+        "metric": METRIC,
+        "value": step_flops / (ms * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded N(0,1) draws at Qwen2.5-14B attention shapes; no weights)",
+        "config": {
+            "workload": f"cfg{wl.cfg}: {wl.name}",
+            "layers": wl.n_layers, "n_q_heads": wl.n_q_heads, "n_kv_heads": wl.n_kv_heads,
+            "head_dim": wl.head_dim, "rope_base": wl.rope_base, "page_size": 16,
+            "blocks": nb, "block_len": wl.block_len, "splice_pos": list(wl.splice_pos)[:4],
+            "suffix_queries": wl.n_suffix, "attn_n_past": list(wl.attn_n_past)[:4],
+            "cache_tokens": wl.n_tokens, "v_layout": wl.v_layout, "softcap": wl.softcap,
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "nexus_suffix_attn (attn_bf16_kernel + split combine), per layer",
+            "achieved": attn_tflops,
+            "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": attn_tflops / MFMA_BF16_PEAK_TFLOPS,
+            "traffic": None,
+            "algorithmic_flops_per_launch": fl_layer,
+            "mean_launch_ms": mean["attn"],
+        },
+        "roofline_hbm": {
+            "bound": "hbm",
+            "splice": {"achieved": splice_gbps, "bytes_per_launch": splice_bytes,
+                       "mean_launch_ms": mean["splice"], "frac": splice_gbps / HBM_PEAK_GBPS},
+            "rephase": {"achieved": rephase_gbps, "bytes_per_launch": rephase_bytes,
+                        "mean_launch_ms": mean["rephase"], "frac": rephase_gbps / HBM_PEAK_GBPS},
+            "rephase_plus_splice_GBps": rs_gbps,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": rs_gbps / HBM_PEAK_GBPS,
+        },
+    }
+    try:
+        res["git"] = subprocess.run(["git", "-C", ROOT, "rev-parse", "--short", "HEAD"],
+                                    capture_output=True, text=True).stdout.strip() or None
+    except Exception:
+        res["git"] = None
+    if args.cpu_kv_sample > 0:
+        print("bench: timing the oracle baseline on the host", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(args.config, min(args.cpu_kv_sample, wl.n_kv_heads))
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,213 @@
+/*
+ * nexus.h - C ABI of the MI355X (gfx950) KV-block splice path.
+ *
+ * The path transplants a precompiled KV block (the keys and values of a tool schema, compiled
+ * once at a RoPE anchor m0) into a live paged KV cache and repairs the seam, following
+ * "Nexus: Depth-Adaptive KV-Cache Splicing" (arXiv 2608.20397):
+ *
+ *   1. nexus_splice_pages      write the block's K/V rows into the cache at a logical cursor
+ *                              (Sec. VI-A; transposed-V caches per Sec. VI-B);
+ *   2. nexus_rephase_k[_paged] re-anchor the block's rotary keys from m0 to the splice position,
+ *                              the exact inverse of the phase drift of eq. (drift) (Sec. III-B);
+ *   3. nexus_suffix_attn       causal grouped-query attention of the re-decoded suffix over the
+ *                              spliced cache (Sec. III-A, Sec. III-C, Sec. VI-A), with optional
+ *                              tanh logit soft-capping and a transposed V cache (Sec. VI-B);
+ *   4. nexus_redecode_len      the redecode length ceil(S * R(n_past) / 100) of eq. (adaptive).
+ *
+ * Conventions shared by every call:
+ *   - Memory: every tensor pointer is a DEVICE pointer unless the argument says "host".  The
+ *     caller owns all memory; the library allocates nothing and keeps no state between calls.
+ *   - Streams: `stream` is a hipStream_t passed as void* (NULL = the null stream).  A call
+ *     validates its arguments on the host, enqueues its kernels on `stream` and returns without
+ *     synchronizing.  Calls on one stream run in order; calls on different streams that touch
+ *     the same memory race.
+ *   - Errors: a status other than NEXUS_OK means nothing was enqueued and nothing was written,
+ *     except NEXUS_EHIP (a HIP launch error; earlier kernels of the same call may have run).
+ *     Faults inside a kernel surface at the caller's next synchronization.  Page-table entries
+ *     live on the device and are not checked by the host: every entry of the logical pages a
+ *     call touches must be in [0, n_phys_pages) (nexus_check_page_table checks a host copy).
+ *   - Element types: bf16 (IEEE-754 binary32 truncated to its top 16 bits) and f32.
+ *   - RoPE: pair i (0 <= i < D/2) of a token at position p is rotated by p * theta_i with
+ *     theta_i = base^(-2i/D) (Sec. III-B).  NEOX pairs features (i, i + D/2); INTERLEAVED pairs
+ *     (2i, 2i + 1).
+ */
+#ifndef NEXUS_H
+#define NEXUS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define NEXUS_ABI_VERSION 1
+
+typedef enum nexus_status {
+  NEXUS_OK = 0,
+  NEXUS_EINVAL = 1,      /* null pointer, non-positive size, unknown enum value              */
+  NEXUS_ESHAPE = 2,      /* head counts, head_dim, layer or page size inconsistent/unsupported */
+  NEXUS_EDTYPE = 3,      /* element type differs between operands or is unsupported          */
+  NEXUS_EROPE = 4,       /* RoPE base / style / anchor differs from the block's header       */
+  NEXUS_ERANGE = 5,      /* a token range or position lies outside the cache or is negative  */
+  NEXUS_ELAYOUT = 6,     /* V layout argument differs from the cache's layout                */
+  NEXUS_EWORKSPACE = 7,  /* workspace missing or smaller than nexus_suffix_attn_workspace()  */
+  NEXUS_EHIP = 8         /* a HIP launch failed                                              */
+} nexus_status;
+
+typedef enum nexus_dtype { NEXUS_BF16 = 0, NEXUS_F32 = 1 } nexus_dtype;
+typedef enum nexus_v_layout { NEXUS_V_ROWMAJOR = 0, NEXUS_V_TRANSPOSED = 1 } nexus_v_layout;
+typedef enum nexus_rope_style { NEXUS_ROPE_NEOX = 0, NEXUS_ROPE_INTERLEAVED = 1 } nexus_rope_style;
+
+/*
+ * A compiled KV block resident in HBM: the device-side counterpart of the paper's compiled
+ * tool block, whose header records the RoPE anchor and parameters (Sec. VI-A).
+ *   k, v        [n_layers][n_tokens][n_kv_heads][head_dim], token-major, contiguous.
+ *   base_pos    RoPE anchor of the keys currently stored in `k` (m0 when freshly compiled);
+ *               nexus_rephase_k updates it.
+ *   rope_base   b of theta_i = b^(-2i/D); rope_style as above.
+ * head_dim must be even; bf16 blocks need head_dim % 16 == 0, f32 blocks head_dim % 8 == 0.
+ */
+typedef struct nexus_block {
+  void *k;
+  void *v;
+  int32_t n_layers, n_tokens, n_kv_heads, head_dim;
+  int32_t dtype;        /* nexus_dtype */
+  int32_t rope_style;   /* nexus_rope_style */
+  int64_t base_pos;
+  double rope_base;
+} nexus_block;
+
+/*
+ * A paged KV cache.  Logical token t lives in physical page map[t / page_size] at slot
+ * t % page_size.
+ *   k  [n_layers][n_phys_pages][n_kv_heads][page_size][head_dim]
+ *   v  ROWMAJOR:   same layout as k
+ *      TRANSPOSED: [n_layers][n_kv_heads][head_dim][n_phys_pages * page_size]; token t is
+ *                  column map[t / page_size] * page_size + t % page_size (the token-innermost
+ *                  V cache of soft-capped models, Sec. VI-B).  With an identity page table
+ *                  this is exactly [kv_head][head_dim][seq].
+ * page_size must be 16.
+ */
+typedef struct nexus_kv_cache {
+  void *k;
+  void *v;
+  int32_t n_layers, n_phys_pages, page_size, n_kv_heads, head_dim;
+  int32_t dtype;        /* nexus_dtype */
+  int32_t v_layout;     /* nexus_v_layout */
+  int32_t rope_style;   /* nexus_rope_style */
+  double rope_base;
+} nexus_kv_cache;
+
+/* Logical -> physical page map, int32 on the device, n_logical_pages entries. */
+typedef struct nexus_page_table {
+  const int32_t *map;
+  int32_t n_logical_pages;
+} nexus_page_table;
+
+/*
+ * Re-anchor every key of a compiled block, in place (Sec. III-B, eq. drift).
+ * Rotates each key pair i of every layer, token and head of block->k by
+ * (dst_pos - src_pos) * theta_i; V is never touched.  The angle is formed and reduced modulo
+ * 2*pi in fp64, its cosine and sine are taken once per pair in fp64 and rounded to fp32, the
+ * rotation is computed in fp32 (bf16 keys) or fp64 (f32 keys) and rounded to nearest-even back
+ * into the block.  dst_pos == src_pos enqueues nothing, leaving the keys bit-identical.
+ * Checks: src_pos == block->base_pos and rope_base == block->rope_base (else NEXUS_EROPE);
+ * positions >= 0 (NEXUS_ERANGE).  On success block->base_pos (a host field) becomes dst_pos.
+ */
+nexus_status nexus_rephase_k(nexus_block *block, int64_t src_pos, int64_t dst_pos,
+                             double rope_base, void *stream);
+
+/*
+ * Re-anchor in place the keys of logical tokens [offset, offset + n_tokens) of every layer and
+ * KV head of a paged cache: the same rotation as nexus_rephase_k, applied where a block was
+ * spliced.  Checks: rope_base == cache->rope_base (NEXUS_EROPE); 0 <= offset and
+ * offset + n_tokens <= pt->n_logical_pages * page_size and pt->n_logical_pages <= n_phys_pages
+ * (NEXUS_ERANGE); n_tokens > 0 (NEXUS_EINVAL).  dst_pos == src_pos enqueues nothing.
+ */
+nexus_status nexus_rephase_k_paged(const nexus_kv_cache *cache, const nexus_page_table *pt,
+                                   int64_t offset, int32_t n_tokens, int64_t src_pos,
+                                   int64_t dst_pos, double rope_base, void *stream);
+
+/*
+ * Splice a block into the cache (Sec. VI-A, Fig. atb; transposed V per Sec. VI-B).
+ * For every layer l, block token j and KV head h, logical slot offset + j of the cache receives
+ * the block's K row (and V row, or V column when the cache is transposed), bit for bit.  No
+ * other cache element is written.  Keys are copied as stored: re-anchor them with
+ * nexus_rephase_k before, or nexus_rephase_k_paged after.
+ * Checks (fail-closed, as the paper validates the block header before any splice): equal
+ * n_layers, n_kv_heads, head_dim (NEXUS_ESHAPE) and dtype (NEXUS_EDTYPE); equal rope_base and
+ * rope_style (NEXUS_EROPE); 0 <= offset, offset + n_tokens within the mapped logical pages
+ * (NEXUS_ERANGE).
+ */
+nexus_status nexus_splice_pages(const nexus_kv_cache *cache, const nexus_page_table *pt,
+                                const nexus_block *block, int64_t offset, void *stream);
+
+/*
+ * Causal grouped-query attention of the re-decoded suffix (Sec. III-A; the suffix of Sec. VI-A).
+ *   q        [n_s][n_q_heads][head_dim] of the cache dtype; query i sits at absolute position
+ *            n_past + i and is already rotated.  Keys are read from layer `layer` of the cache
+ *            through `pt`; the suffix's own keys must already be in the cache.
+ *   n_past   cache tokens before the first suffix query.  Query i attends to keys
+ *            0 .. n_past + i (inclusive).
+ *   Query head h reads KV head h / (n_q_heads / n_kv_heads).
+ *   scale    score scale; 0 selects 1/sqrt(head_dim).
+ *   softcap  0 disables; otherwise score s becomes softcap * tanh(s / softcap) after scaling.
+ *   v_layout must equal cache->v_layout (NEXUS_ELAYOUT).
+ *   out      [n_s][n_q_heads][head_dim] of the cache dtype.
+ *   workspace / workspace_bytes: device scratch of at least nexus_suffix_attn_workspace()
+ *            bytes (may be NULL when that is 0).  Its contents on entry do not matter.
+ * bf16 caches run on MFMA with fp32 accumulation and need head_dim in {64, 128, 256}; f32
+ * caches run an fp32 kernel and need head_dim <= 256.
+ */
+nexus_status nexus_suffix_attn(const void *q, int32_t n_s, int32_t n_q_heads,
+                               const nexus_kv_cache *cache, const nexus_page_table *pt,
+                               int32_t layer, int64_t n_past, float softcap, int32_t v_layout,
+                               float scale, void *out, void *workspace, size_t workspace_bytes,
+                               void *stream);
+
+/* Workspace bytes nexus_suffix_attn needs for these arguments (0 if none, SIZE_MAX if the
+ * arguments are invalid). */
+size_t nexus_suffix_attn_workspace(int32_t n_s, int32_t n_q_heads, const nexus_kv_cache *cache,
+                                   int64_t n_past);
+
+/*
+ * Several suffixes over one cache in one launch (many blocks spliced into one context, each
+ * re-decoding its own tail).  Sequence b has seq_len[b] queries, rows q_start[b] ..
+ * q_start[b] + seq_len[b] - 1 of q and out, at positions seq_n_past[b] + i.  seq_* are HOST
+ * arrays of n_seqs entries (n_seqs <= 32); other arguments as nexus_suffix_attn.
+ */
+nexus_status nexus_suffix_attn_varlen(const void *q, int32_t n_seqs, const int32_t *q_start,
+                                      const int32_t *seq_len, const int64_t *seq_n_past,
+                                      int32_t n_q_heads, const nexus_kv_cache *cache,
+                                      const nexus_page_table *pt, int32_t layer, float softcap,
+                                      int32_t v_layout, float scale, void *out, void *workspace,
+                                      size_t workspace_bytes, void *stream);
+
+size_t nexus_suffix_attn_varlen_workspace(int32_t n_seqs, const int32_t *q_start,
+                                          const int32_t *seq_len, const int64_t *seq_n_past,
+                                          int32_t n_q_heads, const nexus_kv_cache *cache);
+
+/*
+ * Redecode length of eq. (adaptive): ceil(S * R(n_past) / 100) with R = r_base for n_past <= M
+ * and R = r_base + (n_past - M) / (M (K - 1)) * (100 - r_base) above, clamped to 100 (Sec. III-C;
+ * the suffix length of Sec. VI-A).  Exact integer arithmetic.  Host only; returns -1 unless
+ * S >= 0, n_past >= 0, M > 0, 0 <= r_base_pct <= 100 and K >= 2.
+ */
+int64_t nexus_redecode_len(int64_t S, int64_t n_past, int32_t M, int32_t r_base_pct, int32_t K);
+
+/* Host check of a host copy of a page map: entries in [0, n_phys_pages) and pairwise distinct.
+ * Returns NEXUS_OK, NEXUS_EINVAL (null / bad sizes) or NEXUS_ERANGE. */
+nexus_status nexus_check_page_table(const int32_t *host_map, int32_t n_logical_pages,
+                                    int32_t n_phys_pages);
+
+/* Static text for a status code. */
+const char *nexus_status_str(int32_t status);
+
+/* NEXUS_ABI_VERSION of the built library. */
+int32_t nexus_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NEXUS_H */

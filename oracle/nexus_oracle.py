@@ -234,6 +234,22 @@ def rephase_paged(cache_k_values: np.ndarray, page_map: np.ndarray, page_size: i
     return out
 
 
+def rephase_paged_bits(cache_k_bits: np.ndarray, dtype: str, page_map: np.ndarray,
+                       page_size: int, offset: int, n_tokens: int, src_pos: int, dst_pos: int,
+                       base: float, style: str = NEOX) -> np.ndarray:
+    """``rephase_paged`` on raw storage bits: each re-anchored key row is rounded to nearest-even
+    back into the storage type (the stored block is F16/bf16, Sec. VI-A); every other bit of the
+    cache is returned unchanged."""
+    out = np.array(cache_k_bits, copy=True)
+    for t in range(offset, offset + n_tokens):
+        page = int(page_map[t // page_size])
+        slot = t % page_size
+        rows = storage_to_f64(out[:, page, :, slot, :], dtype)
+        out[:, page, :, slot, :] = round_to_storage(
+            rephase(rows, src_pos, dst_pos, base, style), dtype)
+    return out
+
+
 # --------------------------------------------------------------------------------------
 # Suffix-redecode attention (Sec. III-A; soft-cap per Sec. VI-B's soft-capped family)
 # --------------------------------------------------------------------------------------

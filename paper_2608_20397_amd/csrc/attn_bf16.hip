@@ -1,0 +1,567 @@
+// bf16 causal grouped-query suffix attention on gfx950 MFMA (Sec. III-A; the re-decoded suffix
+// of Sec. VI-A; optional tanh soft-cap and transposed V cache per Sec. VI-B).
+//
+// Work decomposition
+//   A workgroup (4 waves) serves one KV head.  Each wave owns a "task": one query head of the
+//   KV head's group and 32 consecutive queries.  Tasks are ordered query-major, so the 4 waves of
+//   a workgroup need nearly the same key range; the workgroup stages every key tile once in LDS
+//   and all 4 waves read it (the GQA group shares its K/V).  The key axis may be split over
+//   several workgroups; a fixed-order combine kernel then merges the partial (m, l, O).
+//   blockIdx.x % n_kv_heads selects the KV head, so on the 8-XCD MI355X every workgroup of one
+//   KV head lands on the same XCD and its K/V tiles are shared through that XCD's L2.
+//
+// Per 64-key tile and wave (head_dim 128)
+//   S^T (keys x queries) = K . Q^T   with v_mfma_f32_32x32x16_bf16: A = K rows from LDS,
+//                                    B = Q held in registers for the whole kernel.
+//   Each lane then holds 32 scores of one query: the online softmax (log2 domain, fp32) needs
+//   one cross-lane max (lanes l and l^32 share a query) and no other shuffle.
+//   O^T (d x queries) += V^T . P^T  with the same MFMA: B = P^T straight from the score
+//                                    registers (bf16), A = V^T rows from LDS.
+//   The MFMA output layout puts keys {4h..4h+3, 8+4h..8+4h+3} of each 16-key step in lane half
+//   h, so the V^T tile stores each 16-key group with key bits 2 and 3 swapped: every A-operand
+//   read is then one 16-byte LDS read.  K rows and V^T rows are XOR-swizzled in 16-byte
+//   chunks to keep those reads free of bank conflicts.
+#include "device_common.h"
+#include "launch.h"
+
+#include <stdlib.h>
+
+namespace nexus {
+
+constexpr int kMaxSeqs = 32;
+constexpr int kWaves = 4;
+constexpr int kQB = 32;   // queries per wave task
+
+struct SeqPlan {
+  int32_t q_start;     // first row of q / out
+  int32_t len;         // queries
+  int64_t n_past;      // position of the first query
+  int32_t row_begin;   // prefix sum of len over sequences (combine indexing)
+  int32_t first_unit;  // first (task group, split) unit of this sequence
+  int32_t n_tasks;     // group * ceil(len / 32)
+  int32_t n_splits;
+  int32_t split_keys;  // keys per split, a multiple of the key tile
+  int32_t pad_;
+  int64_t ws_off;      // float offset of the partial O of this sequence in the workspace
+  int64_t ml_off;      // float offset of its (m, l) pairs
+};
+
+struct AttnPlan {
+  SeqPlan seq[kMaxSeqs];
+  int32_t n_seqs;
+  int32_t units_per_head;
+  int32_t total_rows;
+  int32_t any_split;
+  size_t ws_bytes;
+};
+
+struct AttnArgs {
+  const uint16_t *q;
+  uint16_t *out;
+  const uint16_t *kc;   // layer base of the K cache
+  const uint16_t *vc;   // layer base of the V cache
+  const int32_t *map;
+  float *ws;
+  int32_t n_q_heads, n_kv_heads, group, n_phys_pages;
+  float scale_log2;     // scale * log2(e)
+  float cap_in;         // scale / softcap
+  float cap_out;        // softcap * log2(e)
+};
+
+namespace {
+
+__device__ __forceinline__ float tanh_fast(float x) {
+  // tanh x = 1 - 2 / (e^{2x} + 1); exp2 overflow to +inf gives 1, underflow to 0 gives -1.
+  const float e = fast_exp2(x * 2.8853900817779268f);  // 2 / ln 2
+  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(e + 1.0f);
+}
+
+// key index within a 16-key group -> its position in the V^T tile (swap bits 2 and 3)
+__device__ __forceinline__ int vt_pos(int k) {
+  return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1);
+}
+
+}  // namespace
+
+template <int D, int KT, bool VT, bool CAP>
+__global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const AttnPlan plan) {
+  constexpr int KCH = D / 8;                        // 16-byte chunks per K row
+  constexpr int KSW = (KCH < 16 ? KCH : 16) - 1;    // K row swizzle mask
+  constexpr int VCH = KT / 8;                       // 16-byte chunks per V^T row
+  constexpr int VSW = VCH - 1;
+  constexpr int NKB = KT / 32;                      // 32-key score blocks per tile
+  constexpr int NDB = D / 32;                       // 32-row blocks of O^T
+  constexpr int NS = D / 16;                        // k-steps of Q K^T
+  __shared__ __align__(16) uint16_t Ks[KT * D];
+  __shared__ __align__(16) uint16_t Vs[D * KT];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int j = lane & 31, hh = lane >> 5;
+  const int kvh = blockIdx.x % a.n_kv_heads;
+  int unit = blockIdx.x / a.n_kv_heads;
+  int b = 0;
+  while (b + 1 < plan.n_seqs && unit >= plan.seq[b + 1].first_unit) ++b;
+  const SeqPlan sp = plan.seq[b];
+  unit -= sp.first_unit;
+  const int split = unit % sp.n_splits;
+  const int tgrp = unit / sp.n_splits;
+  const int G = a.group;
+
+  const int task = tgrp * kWaves + wave;
+  const bool active = task < sp.n_tasks;
+  const int qb = task / G;
+  const int g = task - qb * G;
+  const int q0 = qb * kQB;
+  const int qhead = kvh * G + g;
+  const int last_task = min(tgrp * kWaves + kWaves - 1, sp.n_tasks - 1);
+  const int last_q = min((last_task / G + 1) * kQB, sp.len);
+  const int64_t wg_keys = sp.n_past + last_q;
+  const int64_t k_begin = (int64_t)split * sp.split_keys;
+  const int64_t k_end = min(k_begin + (int64_t)sp.split_keys, wg_keys);
+  const int64_t wave_keys = active ? sp.n_past + min(q0 + kQB, sp.len) : 0;
+  const int64_t qpos0 = sp.n_past + q0;  // position of this wave's query 0
+
+  // Q of this wave as B operands: lane (hh, j) holds Q[q0 + j][16 s + 8 hh .. + 7].
+  bf16x8 qreg[NS];
+  if (active) {
+    const int qi = min(q0 + j, sp.len - 1);
+    const uint16_t *qrow = a.q + ((int64_t)(sp.q_start + qi) * a.n_q_heads + qhead) * D;
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      qreg[s] = *reinterpret_cast<const bf16x8 *>(qrow + 16 * s + 8 * hh);
+  }
+
+  f32x16 o[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
+  float m = -INFINITY, l = 0.f;
+
+  const int64_t hstride = (int64_t)kPage * D;               // one (page, head) slab
+  const int64_t n_cols = (int64_t)a.n_phys_pages * kPage;   // transposed V row length
+
+  // ---- global -> register staging of one tile
+  constexpr int K_ITEMS = KT * KCH / 256;                   // 16-byte K chunks per thread
+  constexpr int V_ITEMS_RM = (KT / 4) * (D / 8);            // (4-token, 8-dim) groups
+  constexpr int V_PER_T_RM = (V_ITEMS_RM + 255) / 256;
+  constexpr int V_ITEMS_T = D * (KT / 8);                   // (dim, 8-token) groups
+  constexpr int V_PER_T_T = V_ITEMS_T / 256;
+  static_assert(K_ITEMS >= 1 && KT * KCH % 256 == 0, "tile too small");
+  uint4 kreg[K_ITEMS];
+  uint4 vreg[VT ? V_PER_T_T : 4 * V_PER_T_RM];
+
+  auto load_tile = [&](int64_t kt) {
+#pragma unroll
+    for (int i = 0; i < K_ITEMS; ++i) {
+      const int u = tid + 256 * i;
+      const int key = u / KCH, c = u % KCH;
+      const int64_t t = kt + key;
+      if (t < k_end) {
+        const int64_t page = a.map[t >> kPageShift];
+        kreg[i] = *reinterpret_cast<const uint4 *>(
+            a.kc + (page * a.n_kv_heads + kvh) * hstride + (t & (kPage - 1)) * D + c * 8);
+      } else {
+        kreg[i] = make_uint4(0, 0, 0, 0);
+      }
+    }
+    if constexpr (!VT) {
+#pragma unroll
+      for (int i = 0; i < V_PER_T_RM; ++i) {
+        const int u = tid + 256 * i;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          uint4 val = make_uint4(0, 0, 0, 0);
+          if (u < V_ITEMS_RM) {
+            const int tg4 = u / (D / 8), dc = u % (D / 8);
+            const int64_t t = kt + 4 * tg4 + e;
+            if (t < k_end) {
+              const int64_t page = a.map[t >> kPageShift];
+              val = *reinterpret_cast<const uint4 *>(
+                  a.vc + (page * a.n_kv_heads + kvh) * hstride + (t & (kPage - 1)) * D + dc * 8);
+            }
+          }
+          vreg[4 * i + e] = val;
+        }
+      }
+    } else {
+      const uint16_t *vrow0 = a.vc + (int64_t)kvh * D * n_cols;
+#pragma unroll
+      for (int i = 0; i < V_PER_T_T; ++i) {
+        const int u = tid + 256 * i;
+        const int d = u / (KT / 8), grp = u % (KT / 8);
+        const int64_t t0 = kt + 8 * grp;
+        uint4 val = make_uint4(0, 0, 0, 0);
+        if (t0 + 8 <= k_end) {
+          const int64_t page = a.map[t0 >> kPageShift];
+          val = *reinterpret_cast<const uint4 *>(vrow0 + (int64_t)d * n_cols + page * kPage +
+                                                 (t0 & (kPage - 1)));
+        } else if (t0 < k_end) {
+          const int64_t page = a.map[t0 >> kPageShift];
+          const uint16_t *src = vrow0 + (int64_t)d * n_cols + page * kPage + (t0 & (kPage - 1));
+          uint32_t w[4] = {0, 0, 0, 0};
+          for (int e = 0; e < 8; ++e)
+            if (t0 + e < k_end) w[e >> 1] |= (uint32_t)src[e] << (16 * (e & 1));
+          val = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+        vreg[i] = val;
+      }
+    }
+  };
+
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < K_ITEMS; ++i) {
+      const int u = tid + 256 * i;
+      const int key = u / KCH, c = u % KCH;
+      *reinterpret_cast<uint4 *>(Ks + key * D + ((c ^ (key & KSW)) * 8)) = kreg[i];
+    }
+    if constexpr (!VT) {
+#pragma unroll
+      for (int i = 0; i < V_PER_T_RM; ++i) {
+        const int u = tid + 256 * i;
+        if (u < V_ITEMS_RM) {
+          const int tg4 = u / (D / 8), dc = u % (D / 8);
+          const int pos = (4 * tg4 & ~15) | vt_pos(4 * tg4 & 15);   // 4-aligned
+          const int cc = pos >> 3, half = (pos >> 2) & 1;
+          const uint32_t *w0 = reinterpret_cast<const uint32_t *>(&vreg[4 * i + 0]);
+          const uint32_t *w1 = reinterpret_cast<const uint32_t *>(&vreg[4 * i + 1]);
+          const uint32_t *w2 = reinterpret_cast<const uint32_t *>(&vreg[4 * i + 2]);
+          const uint32_t *w3 = reinterpret_cast<const uint32_t *>(&vreg[4 * i + 3]);
+#pragma unroll
+          for (int dd = 0; dd < 8; ++dd) {
+            const int wi = dd >> 1;
+            uint32_t lo, hi;
+            if (dd & 1) {
+              lo = (w0[wi] >> 16) | (w1[wi] & 0xFFFF0000u);
+              hi = (w2[wi] >> 16) | (w3[wi] & 0xFFFF0000u);
+            } else {
+              lo = (w0[wi] & 0xFFFFu) | (w1[wi] << 16);
+              hi = (w2[wi] & 0xFFFFu) | (w3[wi] << 16);
+            }
+            const int d = 8 * dc + dd;
+            *reinterpret_cast<uint2 *>(Vs + d * KT + ((cc ^ (d & VSW)) * 8) + half * 4) =
+                make_uint2(lo, hi);
+          }
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < V_PER_T_T; ++i) {
+        const int u = tid + 256 * i;
+        const int d = u / (KT / 8), grp = u % (KT / 8);
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int k4 = 8 * grp + 4 * hf;
+          const int pos = (k4 & ~15) | vt_pos(k4 & 15);
+          const int cc = pos >> 3, half = (pos >> 2) & 1;
+          const uint2 piece = hf ? make_uint2(vreg[i].z, vreg[i].w) : make_uint2(vreg[i].x, vreg[i].y);
+          *reinterpret_cast<uint2 *>(Vs + d * KT + ((cc ^ (d & VSW)) * 8) + half * 4) = piece;
+        }
+      }
+    }
+  };
+
+  if (k_begin < k_end) load_tile(k_begin);
+  for (int64_t kt = k_begin; kt < k_end; kt += KT) {
+    __syncthreads();
+    store_tile();
+    __syncthreads();
+    if (kt + KT < k_end) load_tile(kt + KT);
+    if (!active || kt >= wave_keys) continue;
+
+    // ---- S^T = K . Q^T
+    f32x16 sacc[NKB];
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sacc[kb][v] = 0.f;
+      const int key = 32 * kb + j;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const bf16x8 ka =
+            *reinterpret_cast<const bf16x8 *>(Ks + key * D + (((2 * s + hh) ^ (key & KSW)) * 8));
+        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[s], sacc[kb], 0, 0, 0);
+      }
+    }
+
+    // ---- scores in log2 units, masking, online softmax
+    const bool need_mask = (kt + KT > k_end) || (kt + KT - 1 > qpos0);
+    const int64_t my_pos = qpos0 + j;
+    float mt = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float x;
+        if constexpr (CAP) x = a.cap_out * tanh_fast(sacc[kb][v] * a.cap_in);
+        else x = sacc[kb][v] * a.scale_log2;
+        if (need_mask) {
+          const int64_t key = kt + 32 * kb + 8 * (v >> 2) + 4 * hh + (v & 3);
+          if (key >= k_end || key > my_pos) x = -INFINITY;
+        }
+        sacc[kb][v] = x;
+        mt = fmaxf(mt, x);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    const float m_new = fmaxf(m, mt);
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = fast_exp2(m - m_use);
+    float psum = 0.f;
+    bf16x8 pb[NKB][2];
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        float p[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          p[e] = fast_exp2(sacc[kb][8 * hf + e] - m_use);
+          psum += p[e];
+        }
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(p[2 * e], p[2 * e + 1]);
+        pb[kb][hf] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
+      }
+    l = l * alpha + psum;
+    m = m_new;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+
+    // ---- O^T += V^T . P^T
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const int ks = 2 * kb + hf;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const int d = 32 * db + j;
+          const bf16x8 va = *reinterpret_cast<const bf16x8 *>(
+              Vs + d * KT + (((2 * ks + hh) ^ (d & VSW)) * 8));
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kb][hf], o[db], 0, 0, 0);
+        }
+      }
+  }
+
+  // ---- epilogue
+  const float l_tot = l + __shfl_xor(l, 32);
+  if (!active || q0 + j >= sp.len) return;
+  const int row = q0 + j;  // within the sequence
+  if (sp.n_splits == 1) {
+    const float inv = 1.0f / l_tot;
+    uint16_t *orow = a.out + ((int64_t)(sp.q_start + row) * a.n_q_heads + qhead) * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        const int d0 = 32 * db + 8 * gq + 4 * hh;
+        const uint32_t lo = pack_bf16x2(o[db][4 * gq + 0] * inv, o[db][4 * gq + 1] * inv);
+        const uint32_t hi = pack_bf16x2(o[db][4 * gq + 2] * inv, o[db][4 * gq + 3] * inv);
+        *reinterpret_cast<uint2 *>(orow + d0) = make_uint2(lo, hi);
+      }
+  } else {
+    const int64_t prow = ((int64_t)split * sp.len + row) * a.n_q_heads + qhead;
+    float *op = a.ws + sp.ws_off + prow * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        const int d0 = 32 * db + 8 * gq + 4 * hh;
+        *reinterpret_cast<float4 *>(op + d0) =
+            make_float4(o[db][4 * gq + 0], o[db][4 * gq + 1], o[db][4 * gq + 2], o[db][4 * gq + 3]);
+      }
+    if (hh == 0) *reinterpret_cast<float2 *>(a.ws + sp.ml_off + prow * 2) = make_float2(m, l_tot);
+  }
+}
+
+// Fixed-order merge of the split partials: m = max m_s, w_s = 2^(m_s - m),
+// out = sum_s w_s O_s / sum_s w_s l_s.  One thread per 4 output features.
+template <int D>
+__global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a, const AttnPlan plan) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  constexpr int Q4 = D / 4;
+  const int64_t total = (int64_t)plan.total_rows * a.n_q_heads * Q4;
+  if (gid >= total) return;
+  const int d4 = (int)(gid % Q4);
+  const int64_t rh = gid / Q4;
+  const int head = (int)(rh % a.n_q_heads);
+  const int rowg = (int)(rh / a.n_q_heads);
+  int b = 0;
+  while (b + 1 < plan.n_seqs && rowg >= plan.seq[b + 1].row_begin) ++b;
+  const SeqPlan sp = plan.seq[b];
+  if (sp.n_splits == 1) return;
+  const int row = rowg - sp.row_begin;
+  float mmax = -INFINITY;
+  for (int s = 0; s < sp.n_splits; ++s) {
+    const int64_t prow = ((int64_t)s * sp.len + row) * a.n_q_heads + head;
+    mmax = fmaxf(mmax, a.ws[sp.ml_off + prow * 2]);
+  }
+  float lsum = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s = 0; s < sp.n_splits; ++s) {
+    const int64_t prow = ((int64_t)s * sp.len + row) * a.n_q_heads + head;
+    const float2 ml = *reinterpret_cast<const float2 *>(a.ws + sp.ml_off + prow * 2);
+    const float w = (ml.x == -INFINITY) ? 0.f : fast_exp2(ml.x - mmax);
+    lsum += w * ml.y;
+    const float4 ov = *reinterpret_cast<const float4 *>(a.ws + sp.ws_off + prow * D + 4 * d4);
+    acc.x += w * ov.x;
+    acc.y += w * ov.y;
+    acc.z += w * ov.z;
+    acc.w += w * ov.w;
+  }
+  const float inv = 1.0f / lsum;
+  uint16_t *orow = a.out + ((int64_t)(sp.q_start + row) * a.n_q_heads + head) * D + 4 * d4;
+  *reinterpret_cast<uint2 *>(orow) =
+      make_uint2(pack_bf16x2(acc.x * inv, acc.y * inv), pack_bf16x2(acc.z * inv, acc.w * inv));
+}
+
+namespace {
+
+int key_tile_for(int head_dim) { return head_dim >= 256 ? 32 : 64; }
+
+int target_workgroups() {
+  static int t = [] {
+    const char *e = getenv("NEXUS_ATTN_TARGET_WGS");
+    const int v = e ? atoi(e) : 0;
+    return v > 0 ? v : 1024;
+  }();
+  return t;
+}
+
+// Deterministic plan of an attention launch: task groups, key splits and workspace offsets.
+// The same arguments always give the same plan (the workspace query relies on it).
+bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
+  if (p.n_seqs < 1 || p.n_seqs > kMaxSeqs) return false;
+  const int G = p.n_q_heads / p.n_kv_heads;
+  const int KT = key_tile_for(p.head_dim);
+  plan = AttnPlan{};
+  plan.n_seqs = p.n_seqs;
+  double key_work = 0;
+  int64_t groups = 0;
+  for (int b = 0; b < p.n_seqs; ++b) {
+    const AttnSeq &s = p.seqs[b];
+    const int n_tasks = G * ((s.len + kQB - 1) / kQB);
+    const int n_tg = (n_tasks + kWaves - 1) / kWaves;
+    key_work += (double)n_tg * (double)(s.n_past + s.len);
+    groups += n_tg;
+  }
+  const double per_wg = key_work * p.n_kv_heads / target_workgroups();
+  int64_t split_keys = (int64_t)per_wg;
+  if (split_keys < 1024) split_keys = 1024;
+  split_keys = (split_keys + KT - 1) / KT * KT;
+  int32_t unit = 0, rows = 0;
+  int64_t ws_floats = 0;
+  for (int b = 0; b < p.n_seqs; ++b) {
+    const AttnSeq &s = p.seqs[b];
+    SeqPlan &sp = plan.seq[b];
+    sp.q_start = s.q_start;
+    sp.len = s.len;
+    sp.n_past = s.n_past;
+    sp.row_begin = rows;
+    sp.first_unit = unit;
+    sp.n_tasks = G * ((s.len + kQB - 1) / kQB);
+    const int n_tg = (sp.n_tasks + kWaves - 1) / kWaves;
+    const int64_t keys = s.n_past + s.len;
+    int64_t ns = (keys + split_keys - 1) / split_keys;
+    if (ns < 1) ns = 1;
+    // balance the splits: equal key counts rounded to the tile
+    int64_t sk = (keys + ns - 1) / ns;
+    sk = (sk + KT - 1) / KT * KT;
+    ns = (keys + sk - 1) / sk;
+    sp.n_splits = (int32_t)ns;
+    sp.split_keys = (int32_t)sk;
+    unit += n_tg * sp.n_splits;
+    rows += s.len;
+    if (sp.n_splits > 1) {
+      plan.any_split = 1;
+      sp.ws_off = ws_floats;
+      ws_floats += (int64_t)sp.n_splits * s.len * p.n_q_heads * p.head_dim;
+      sp.ml_off = ws_floats;
+      ws_floats += (int64_t)sp.n_splits * s.len * p.n_q_heads * 2;
+    }
+  }
+  plan.units_per_head = unit;
+  plan.total_rows = rows;
+  plan.ws_bytes = (size_t)ws_floats * sizeof(float);
+  (void)groups;
+  return true;
+}
+
+template <int D, int KT, bool VT, bool CAP>
+void launch_main(const AttnArgs &args, const AttnPlan &plan, int n_kv, hipStream_t stream) {
+  hipLaunchKernelGGL((attn_bf16_kernel<D, KT, VT, CAP>), dim3(plan.units_per_head * n_kv),
+                     dim3(256), 0, stream, args, plan);
+}
+
+template <int D, int KT>
+void dispatch_main(const AttnArgs &args, const AttnPlan &plan, int n_kv, bool vt, bool cap,
+                   hipStream_t stream) {
+  if (vt) {
+    if (cap) launch_main<D, KT, true, true>(args, plan, n_kv, stream);
+    else launch_main<D, KT, true, false>(args, plan, n_kv, stream);
+  } else {
+    if (cap) launch_main<D, KT, false, true>(args, plan, n_kv, stream);
+    else launch_main<D, KT, false, false>(args, plan, n_kv, stream);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attention_f32(const AttnLaunch &p, hipStream_t stream);
+
+size_t attn_workspace_bytes(const AttnLaunch &p) {
+  if (!p.is_bf16) return 0;
+  AttnPlan plan;
+  if (!make_plan(p, plan)) return (size_t)-1;
+  return plan.ws_bytes;
+}
+
+hipError_t launch_attention(const AttnLaunch &p, hipStream_t stream) {
+  if (!p.is_bf16) return launch_attention_f32(p, stream);
+  AttnPlan plan;
+  if (!make_plan(p, plan)) return hipErrorInvalidValue;
+  if (plan.ws_bytes > p.workspace_bytes) return hipErrorInvalidValue;
+  AttnArgs args;
+  const int64_t layer_elems = (int64_t)p.n_phys_pages * p.n_kv_heads * kPage * p.head_dim;
+  args.q = (const uint16_t *)p.q;
+  args.out = (uint16_t *)p.out;
+  args.kc = (const uint16_t *)p.cache_k + (int64_t)p.layer * layer_elems;
+  args.vc = (const uint16_t *)p.cache_v + (int64_t)p.layer * layer_elems;
+  args.map = p.map;
+  args.ws = (float *)p.workspace;
+  args.n_q_heads = p.n_q_heads;
+  args.n_kv_heads = p.n_kv_heads;
+  args.group = p.n_q_heads / p.n_kv_heads;
+  args.n_phys_pages = p.n_phys_pages;
+  const float log2e = 1.4426950408889634f;
+  args.scale_log2 = p.scale * log2e;
+  args.cap_in = p.softcap > 0.f ? p.scale / p.softcap : 0.f;
+  args.cap_out = p.softcap * log2e;
+  const bool cap = p.softcap > 0.f;
+  switch (p.head_dim) {
+    case 64: dispatch_main<64, 64>(args, plan, p.n_kv_heads, p.v_transposed, cap, stream); break;
+    case 128: dispatch_main<128, 64>(args, plan, p.n_kv_heads, p.v_transposed, cap, stream); break;
+    case 256: dispatch_main<256, 32>(args, plan, p.n_kv_heads, p.v_transposed, cap, stream); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (plan.any_split) {
+    const int64_t total = (int64_t)plan.total_rows * p.n_q_heads * (p.head_dim / 4);
+    const uint32_t blocks = (uint32_t)((total + 255) / 256);
+    switch (p.head_dim) {
+      case 64: hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(blocks), dim3(256), 0, stream, args, plan); break;
+      case 128: hipLaunchKernelGGL(attn_combine_kernel<128>, dim3(blocks), dim3(256), 0, stream, args, plan); break;
+      case 256: hipLaunchKernelGGL(attn_combine_kernel<256>, dim3(blocks), dim3(256), 0, stream, args, plan); break;
+    }
+    e = hipGetLastError();
+  }
+  return e;
+}
+
+}  // namespace nexus

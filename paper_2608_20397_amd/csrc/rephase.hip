@@ -1,0 +1,207 @@
+// Re-anchoring of rotary keys (Sec. III-B): every key pair i of the selected rows is rotated
+// by delta * theta_i, theta_i = base^(-2i/D), delta = splice position - compile anchor
+// (the inverse of the drift of eq. (drift)).  In place; V is never touched.
+//
+// HBM-bound: each thread owns a fixed group of feature pairs, forms their angles once in fp64
+// (reduced modulo 2*pi in fp64, cosine and sine in fp64 rounded to fp32), keeps cos/sin in
+// registers, and then streams rows with 16-byte loads and stores.  bf16 keys rotate in fp32 and
+// round to nearest-even; f32 keys rotate in fp64 and round once.
+#include "device_common.h"
+#include "launch.h"
+
+namespace nexus {
+
+namespace {
+
+constexpr double kTwoPiHi = 6.283185307179586232;       // fp64(2*pi)
+constexpr double kTwoPiLo = 2.4492935982947064e-16;     // 2*pi - fp64(2*pi)
+
+__device__ __forceinline__ void pair_angle(int64_t delta, double base, int i, int head_dim,
+                                           double &c, double &s) {
+  const double theta = pow(base, -2.0 * (double)i / (double)head_dim);
+  const double ang = (double)delta * theta;
+  const double k = rint(ang / kTwoPiHi);
+  double r = fma(-k, kTwoPiHi, ang);
+  r = fma(-k, kTwoPiLo, r);
+  sincos(r, &s, &c);
+}
+
+template <typename T>
+struct Pack;  // 16 bytes of keys
+
+template <>
+struct Pack<uint16_t> {  // 8 bf16
+  static constexpr int N = 8;
+  __device__ static void unpack(const uint4 &v, float *x) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = __uint_as_float(w[e] << 16);
+      x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
+  }
+  __device__ static uint4 pack(const float *x) {
+    uint4 v;
+    v.x = pack_bf16x2(x[0], x[1]);
+    v.y = pack_bf16x2(x[2], x[3]);
+    v.z = pack_bf16x2(x[4], x[5]);
+    v.w = pack_bf16x2(x[6], x[7]);
+    return v;
+  }
+};
+
+template <>
+struct Pack<uint32_t> {  // 4 f32
+  static constexpr int N = 4;
+  __device__ static void unpack(const uint4 &v, float *x) {
+    x[0] = __uint_as_float(v.x);
+    x[1] = __uint_as_float(v.y);
+    x[2] = __uint_as_float(v.z);
+    x[3] = __uint_as_float(v.w);
+  }
+  __device__ static uint4 pack(const float *x) {
+    return make_uint4(__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]),
+                      __float_as_uint(x[3]));
+  }
+};
+
+// Rotate pairs (a[e], b[e]) by (c[e], s[e]).
+template <typename T>
+__device__ __forceinline__ void rotate(float *a, float *b, const float *c, const float *s,
+                                       const double *cd, const double *sd) {
+  constexpr int N = Pack<T>::N;
+#pragma unroll
+  for (int e = 0; e < N; ++e) {
+    if constexpr (sizeof(T) == 2) {
+      const float xa = a[e], xb = b[e];
+      a[e] = xa * c[e] - xb * s[e];
+      b[e] = xa * s[e] + xb * c[e];
+    } else {
+      const double xa = a[e], xb = b[e];
+      a[e] = (float)(xa * cd[e] - xb * sd[e]);
+      b[e] = (float)(xa * sd[e] + xb * cd[e]);
+    }
+  }
+}
+
+}  // namespace
+
+// NEOX: thread chunk c owns pairs [N c, N c + N): elements [N c, +N) and [D/2 + N c, +N).
+// INTERLEAVED: thread chunk c owns elements [2 N c, 2 N c + 2 N) = pairs [N c, N c + N).
+template <typename T, bool INTERLEAVED>
+__global__ __launch_bounds__(256) void rephase_kernel(
+    T *__restrict__ k, const int32_t *__restrict__ map, int64_t offset, uint32_t n_rows,
+    uint32_t tpr_shift, FastDiv div_heads, FastDiv div_layer_rows, uint32_t n_heads,
+    uint32_t n_tokens, uint32_t n_phys_pages, int32_t head_dim, int64_t delta, double base) {
+  constexpr int N = Pack<T>::N;
+  const uint32_t tpr = 1u << tpr_shift;  // threads per row
+  const uint32_t gtid = blockIdx.x * blockDim.x + threadIdx.x;
+  const uint32_t c = gtid & (tpr - 1);
+  const uint32_t row_step = (gridDim.x * blockDim.x) >> tpr_shift;
+
+  float cf[N], sf[N];
+  double cd[N], sd[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) {
+    pair_angle(delta, base, (int)(N * c + e), head_dim, cd[e], sd[e]);
+    cf[e] = (float)cd[e];
+    sf[e] = (float)sd[e];
+  }
+
+  for (uint32_t r = gtid >> tpr_shift; r < n_rows; r += row_step) {
+    T *row;
+    if (map == nullptr) {
+      row = k + (uint64_t)r * head_dim;
+    } else {
+      const uint32_t l = fdiv(r, div_layer_rows);
+      const uint32_t rem = r - l * n_tokens * n_heads;
+      const uint32_t j = fdiv(rem, div_heads);
+      const uint32_t h = rem - j * n_heads;
+      const int64_t t = offset + j;
+      const uint64_t page = (uint32_t)map[t >> kPageShift];
+      row = k + ((((uint64_t)l * n_phys_pages + page) * n_heads + h) * kPage +
+                 (uint64_t)(t & (kPage - 1))) * head_dim;
+    }
+    uint4 *pa, *pb;
+    if constexpr (INTERLEAVED) {
+      pa = reinterpret_cast<uint4 *>(row + 2 * N * c);
+      pb = pa + 1;
+    } else {
+      pa = reinterpret_cast<uint4 *>(row + N * c);
+      pb = reinterpret_cast<uint4 *>(row + head_dim / 2 + N * c);
+    }
+    const uint4 va = *pa, vb = *pb;
+    float x[2 * N], a[N], b[N];
+    Pack<T>::unpack(va, x);
+    Pack<T>::unpack(vb, x + N);
+    if constexpr (INTERLEAVED) {
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        a[e] = x[2 * e];
+        b[e] = x[2 * e + 1];
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        a[e] = x[e];
+        b[e] = x[N + e];
+      }
+    }
+    rotate<T>(a, b, cf, sf, cd, sd);
+    if constexpr (INTERLEAVED) {
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        x[2 * e] = a[e];
+        x[2 * e + 1] = b[e];
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        x[e] = a[e];
+        x[N + e] = b[e];
+      }
+    }
+    *pa = Pack<T>::pack(x);
+    *pb = Pack<T>::pack(x + N);
+  }
+}
+
+hipError_t launch_rephase(const RephaseLaunch &p, hipStream_t stream) {
+  const int n_per16 = 16 / p.dtype_bytes;                // pairs per thread
+  const uint32_t tpr = (uint32_t)(p.head_dim / 2 / n_per16);
+  uint32_t shift = 0;
+  while ((1u << shift) < tpr) ++shift;
+  const uint64_t rows = (uint64_t)p.n_layers * p.n_tokens * p.n_heads;
+  const uint64_t threads_needed = rows << shift;
+  uint64_t blocks = (threads_needed + 256 * 4 - 1) / (256 * 4);   // ~4 rows per thread
+  if (blocks < 1) blocks = 1;
+  if (blocks > 1u << 20) blocks = 1u << 20;
+  const FastDiv dh = make_fastdiv((uint32_t)p.n_heads);
+  const FastDiv dl = make_fastdiv((uint32_t)(p.n_tokens * p.n_heads));
+  if (p.dtype_bytes == 2) {
+    if (p.interleaved)
+      hipLaunchKernelGGL((rephase_kernel<uint16_t, true>), dim3((uint32_t)blocks), dim3(256), 0,
+                         stream, (uint16_t *)p.k, p.map, p.offset, (uint32_t)rows, shift, dh, dl,
+                         (uint32_t)p.n_heads, (uint32_t)p.n_tokens, (uint32_t)p.n_phys_pages,
+                         p.head_dim, p.delta, p.rope_base);
+    else
+      hipLaunchKernelGGL((rephase_kernel<uint16_t, false>), dim3((uint32_t)blocks), dim3(256), 0,
+                         stream, (uint16_t *)p.k, p.map, p.offset, (uint32_t)rows, shift, dh, dl,
+                         (uint32_t)p.n_heads, (uint32_t)p.n_tokens, (uint32_t)p.n_phys_pages,
+                         p.head_dim, p.delta, p.rope_base);
+  } else {
+    if (p.interleaved)
+      hipLaunchKernelGGL((rephase_kernel<uint32_t, true>), dim3((uint32_t)blocks), dim3(256), 0,
+                         stream, (uint32_t *)p.k, p.map, p.offset, (uint32_t)rows, shift, dh, dl,
+                         (uint32_t)p.n_heads, (uint32_t)p.n_tokens, (uint32_t)p.n_phys_pages,
+                         p.head_dim, p.delta, p.rope_base);
+    else
+      hipLaunchKernelGGL((rephase_kernel<uint32_t, false>), dim3((uint32_t)blocks), dim3(256), 0,
+                         stream, (uint32_t *)p.k, p.map, p.offset, (uint32_t)rows, shift, dh, dl,
+                         (uint32_t)p.n_heads, (uint32_t)p.n_tokens, (uint32_t)p.n_phys_pages,
+                         p.head_dim, p.delta, p.rope_base);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace nexus

@@ -1,0 +1,263 @@
+"""ctypes binding of libnexus (include/nexus.h): argument marshalling only.
+
+Every step of the path runs in the library's HIP kernels.  torch provides device memory and the
+current stream; this module builds the C descriptors from tensors, calls the C entry points on
+``torch.cuda.current_stream()`` and turns a non-zero status into :class:`NexusError`.  If the
+shared library has not been built, :func:`lib` raises: there is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libnexus.so")
+
+OK, EINVAL, ESHAPE, EDTYPE, EROPE, ERANGE, ELAYOUT, EWORKSPACE, EHIP = range(9)
+BF16, F32 = 0, 1
+V_ROWMAJOR, V_TRANSPOSED = 0, 1
+ROPE_NEOX, ROPE_INTERLEAVED = 0, 1
+PAGE = 16
+
+
+class NexusError(RuntimeError):
+    def __init__(self, status: int, what: str = ""):
+        self.status = status
+        msg = lib().nexus_status_str(status).decode()
+        super().__init__(f"{what}: status {status} ({msg})" if what else f"status {status} ({msg})")
+
+
+class CBlock(C.Structure):
+    _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("n_layers", C.c_int32),
+                ("n_tokens", C.c_int32), ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32),
+                ("dtype", C.c_int32), ("rope_style", C.c_int32), ("base_pos", C.c_int64),
+                ("rope_base", C.c_double)]
+
+
+class CKvCache(C.Structure):
+    _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("n_layers", C.c_int32),
+                ("n_phys_pages", C.c_int32), ("page_size", C.c_int32), ("n_kv_heads", C.c_int32),
+                ("head_dim", C.c_int32), ("dtype", C.c_int32), ("v_layout", C.c_int32),
+                ("rope_style", C.c_int32), ("rope_base", C.c_double)]
+
+
+class CPageTable(C.Structure):
+    _fields_ = [("map", C.c_void_p), ("n_logical_pages", C.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libnexus.so (built by ``paper_2608_20397_amd.build``); raise if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2608_20397_amd.build`")
+    L = C.CDLL(LIB_PATH)
+    vp, i32, i64, f32, f64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_float, C.c_double, C.c_size_t
+    pB, pC, pT = C.POINTER(CBlock), C.POINTER(CKvCache), C.POINTER(CPageTable)
+    sigs = {
+        "nexus_abi_version": (i32, []),
+        "nexus_status_str": (C.c_char_p, [i32]),
+        "nexus_redecode_len": (i64, [i64, i64, i32, i32, i32]),
+        "nexus_check_page_table": (i32, [C.POINTER(C.c_int32), i32, i32]),
+        "nexus_rephase_k": (i32, [pB, i64, i64, f64, vp]),
+        "nexus_rephase_k_paged": (i32, [pC, pT, i64, i32, i64, i64, f64, vp]),
+        "nexus_splice_pages": (i32, [pC, pT, pB, i64, vp]),
+        "nexus_suffix_attn": (i32, [vp, i32, i32, pC, pT, i32, i64, f32, i32, f32, vp, vp, sz, vp]),
+        "nexus_suffix_attn_workspace": (sz, [i32, i32, pC, i64]),
+        "nexus_suffix_attn_varlen": (i32, [vp, i32, C.POINTER(C.c_int32), C.POINTER(C.c_int32),
+                                           C.POINTER(C.c_int64), i32, pC, pT, i32, f32, i32, f32,
+                                           vp, vp, sz, vp]),
+        "nexus_suffix_attn_varlen_workspace": (sz, [i32, C.POINTER(C.c_int32),
+                                                    C.POINTER(C.c_int32), C.POINTER(C.c_int64),
+                                                    i32, pC]),
+    }
+    for name, (res, args) in sigs.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(status: int, what: str):
+    if status != OK:
+        raise NexusError(status, what)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise NexusError(EDTYPE, f"unsupported dtype {t.dtype}")
+
+
+def _stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return C.c_void_p(t.data_ptr()) if t is not None else C.c_void_p(0)
+
+
+@dataclass
+class Block:
+    """A compiled KV block in HBM: k, v [n_layers][n_tokens][n_kv_heads][head_dim]."""
+    k: torch.Tensor
+    v: torch.Tensor
+    base_pos: int
+    rope_base: float
+    rope_style: int = ROPE_NEOX
+
+    def c(self) -> CBlock:
+        L, T, H, D = self.k.shape
+        if tuple(self.v.shape) != (L, T, H, D) or not (self.k.is_contiguous() and self.v.is_contiguous()):
+            raise NexusError(ESHAPE, "block k/v must be contiguous [L][T][H][D] of equal shape")
+        return CBlock(self.k.data_ptr(), self.v.data_ptr(), L, T, H, D, _dtype_code(self.k),
+                      self.rope_style, self.base_pos, self.rope_base)
+
+
+@dataclass
+class PagedKVCache:
+    """k [L][n_phys_pages][H][16][D]; v the same or, transposed, [L][H][D][n_phys_pages*16];
+    page_map int32 [n_logical_pages] on the device."""
+    k: torch.Tensor
+    v: torch.Tensor
+    page_map: torch.Tensor
+    rope_base: float
+    v_layout: int = V_ROWMAJOR
+    rope_style: int = ROPE_NEOX
+
+    def c(self) -> CKvCache:
+        L, npp, H, P, D = self.k.shape
+        if P != PAGE or not (self.k.is_contiguous() and self.v.is_contiguous()):
+            raise NexusError(ESHAPE, "cache k must be contiguous [L][pages][H][16][D]")
+        want_v = (L, H, D, npp * P) if self.v_layout == V_TRANSPOSED else (L, npp, H, P, D)
+        if tuple(self.v.shape) != want_v:
+            raise NexusError(ESHAPE, f"cache v must be {want_v}, got {tuple(self.v.shape)}")
+        if self.v.dtype != self.k.dtype:
+            raise NexusError(EDTYPE, "cache k and v dtypes differ")
+        return CKvCache(self.k.data_ptr(), self.v.data_ptr(), L, npp, P, H, D,
+                        _dtype_code(self.k), self.v_layout, self.rope_style, self.rope_base)
+
+    def pt(self) -> CPageTable:
+        if self.page_map.dtype != torch.int32 or not self.page_map.is_contiguous():
+            raise NexusError(EINVAL, "page_map must be contiguous int32")
+        return CPageTable(self.page_map.data_ptr(), self.page_map.numel())
+
+    @property
+    def n_layers(self):
+        return self.k.shape[0]
+
+
+def splice_pages(cache: PagedKVCache, block: Block, offset: int):
+    cc, pt, cb = cache.c(), cache.pt(), block.c()
+    _check(lib().nexus_splice_pages(C.byref(cc), C.byref(pt), C.byref(cb), offset, _stream()),
+           "nexus_splice_pages")
+
+
+def rephase_k(block: Block, src_pos: int, dst_pos: int, rope_base: float):
+    cb = block.c()
+    _check(lib().nexus_rephase_k(C.byref(cb), src_pos, dst_pos, rope_base, _stream()),
+           "nexus_rephase_k")
+    block.base_pos = cb.base_pos
+
+
+def rephase_k_paged(cache: PagedKVCache, offset: int, n_tokens: int, src_pos: int, dst_pos: int,
+                    rope_base: float):
+    cc, pt = cache.c(), cache.pt()
+    _check(lib().nexus_rephase_k_paged(C.byref(cc), C.byref(pt), offset, n_tokens, src_pos,
+                                       dst_pos, rope_base, _stream()), "nexus_rephase_k_paged")
+
+
+def suffix_attn_workspace_bytes(cache: PagedKVCache, n_s: int, n_q_heads: int, n_past: int) -> int:
+    cc = cache.c()
+    n = lib().nexus_suffix_attn_workspace(n_s, n_q_heads, C.byref(cc), n_past)
+    if n == (1 << 64) - 1:
+        raise NexusError(EINVAL, "nexus_suffix_attn_workspace")
+    return n
+
+
+def _workspace(nbytes: int, device, workspace):
+    if nbytes == 0:
+        return None
+    if workspace is not None:
+        return workspace
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def suffix_attn(q: torch.Tensor, cache: PagedKVCache, layer: int, n_past: int,
+                softcap: float = 0.0, v_layout: int | None = None, scale: float = 0.0,
+                out: torch.Tensor | None = None, workspace: torch.Tensor | None = None):
+    """q [n_s][n_q_heads][D] -> out [n_s][n_q_heads][D] (cache dtype)."""
+    n_s, hq, _ = q.shape
+    if not q.is_contiguous():
+        raise NexusError(EINVAL, "q must be contiguous")
+    if q.dtype != cache.k.dtype:
+        raise NexusError(EDTYPE, "q dtype differs from the cache")
+    if out is None:
+        out = torch.empty_like(q)
+    elif out.shape != q.shape or out.dtype != q.dtype or not out.is_contiguous():
+        raise NexusError(EINVAL, "out must be contiguous, shaped and typed like q")
+    cc, pt = cache.c(), cache.pt()
+    ws_bytes = lib().nexus_suffix_attn_workspace(n_s, hq, C.byref(cc), n_past)
+    if ws_bytes == (1 << 64) - 1:
+        raise NexusError(EINVAL, "nexus_suffix_attn_workspace")
+    ws = _workspace(ws_bytes, q.device, workspace)
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().nexus_suffix_attn(_ptr(q), n_s, hq, C.byref(cc), C.byref(pt), layer, n_past,
+                                   softcap, cache.v_layout if v_layout is None else v_layout,
+                                   scale, _ptr(out), _ptr(ws), nbytes, _stream()),
+           "nexus_suffix_attn")
+    return out
+
+
+def suffix_attn_varlen(q: torch.Tensor, q_start, seq_len, seq_n_past, cache: PagedKVCache,
+                       layer: int, softcap: float = 0.0, v_layout: int | None = None,
+                       scale: float = 0.0, out: torch.Tensor | None = None,
+                       workspace: torch.Tensor | None = None):
+    """Several suffixes in one launch: rows q_start[b] .. + seq_len[b] at positions
+    seq_n_past[b] + i."""
+    n = len(seq_len)
+    qs = (C.c_int32 * n)(*q_start)
+    ls = (C.c_int32 * n)(*seq_len)
+    ps = (C.c_int64 * n)(*seq_n_past)
+    _, hq, _ = q.shape
+    if not q.is_contiguous():
+        raise NexusError(EINVAL, "q must be contiguous")
+    if out is None:
+        out = torch.empty_like(q)
+    cc, pt = cache.c(), cache.pt()
+    ws_bytes = lib().nexus_suffix_attn_varlen_workspace(n, qs, ls, ps, hq, C.byref(cc))
+    if ws_bytes == (1 << 64) - 1:
+        raise NexusError(EINVAL, "nexus_suffix_attn_varlen_workspace")
+    ws = _workspace(ws_bytes, q.device, workspace)
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().nexus_suffix_attn_varlen(_ptr(q), n, qs, ls, ps, hq, C.byref(cc), C.byref(pt),
+                                          layer, softcap,
+                                          cache.v_layout if v_layout is None else v_layout,
+                                          scale, _ptr(out), _ptr(ws), nbytes, _stream()),
+           "nexus_suffix_attn_varlen")
+    return out
+
+
+def redecode_len(S: int, n_past: int, M: int = 256, r_base_pct: int = 5, K: int = 4) -> int:
+    r = lib().nexus_redecode_len(S, n_past, M, r_base_pct, K)
+    if r < 0:
+        raise NexusError(EINVAL, "nexus_redecode_len")
+    return r
+
+
+def check_page_table(host_map, n_phys_pages: int) -> None:
+    import numpy as np
+    a = np.ascontiguousarray(np.asarray(host_map, dtype=np.int32))
+    _check(lib().nexus_check_page_table(a.ctypes.data_as(C.POINTER(C.c_int32)), a.size,
+                                        n_phys_pages), "nexus_check_page_table")

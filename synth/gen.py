@@ -109,16 +109,20 @@ class HostCase:
     q: np.ndarray
 
 
-def host_case(cfg: int, layers=None, n_tokens_override=None) -> HostCase:
+def host_case(cfg: int, layers=None) -> HostCase:
     """Draw one config's inputs on the host for the given layers (default: all)."""
-    wl = get_workload(cfg)
+    return host_case_wl(get_workload(cfg), cfg, layers)
+
+
+def host_case_wl(wl: Workload, seed_cfg: int, layers=None) -> HostCase:
+    """Draw inputs for any workload record; ``seed_cfg`` takes the config slot of the seed."""
     layers = list(range(wl.n_layers)) if layers is None else list(layers)
     H, D, Hq = wl.n_kv_heads, wl.head_dim, wl.n_q_heads
-    n_ctx = wl.n_tokens if cfg == 4 else wl.splice_pos[0]
     n_blocks = len(wl.splice_pos)
+    n_ctx = wl.n_tokens if n_blocks > 1 else wl.splice_pos[0]
 
     def draw(tag, shape, std, tag_offset=0):
-        return np.stack([to_bits(normal(cfg, l, tag + tag_offset, shape, std), wl.dtype)
+        return np.stack([to_bits(normal(seed_cfg, l, tag + tag_offset, shape, std), wl.dtype)
                          for l in layers])
 
     ctx_k = draw(TAG["k_ctx"], (n_ctx, H, D), wl.k_scale)
@@ -129,8 +133,8 @@ def host_case(cfg: int, layers=None, n_tokens_override=None) -> HostCase:
     user_k = draw(TAG["k_user"], (wl.n_user, H, D), wl.k_scale)
     user_v = draw(TAG["v_user"], (wl.n_user, H, D), wl.v_scale)
     q = draw(TAG["q"], (wl.n_suffix * n_blocks, Hq, D), wl.q_scale)
-    return HostCase(wl, page_map(cfg, wl.n_pages, wl.shuffled_pages), n_ctx, ctx_k, ctx_v,
-                    blk_k, blk_v, user_k, user_v, q)
+    pm = page_map(seed_cfg, wl.n_pages, wl.shuffled_pages)
+    return HostCase(wl, pm, n_ctx, ctx_k, ctx_v, blk_k, blk_v, user_k, user_v, q)
 
 
 def empty_cache_bits(wl: Workload, n_layers: int, n_phys_pages: int | None = None):

@@ -1,0 +1,173 @@
+"""GPU parity of the suffix attention against the fp64 oracle.
+
+Tolerances: bf16 outputs max-abs 2e-2 and rel-RMS 5e-3 (rel-RMS = ||gpu - oracle||_2 /
+||oracle||_2 over the compared block); f32 outputs 1e-5 for both.  The oracle attends over its
+own cache (its own splice and re-anchor, rounded to the storage type), never the GPU's.
+Full-size configs 3 and 4 run in the launch configuration the benchmark times and are compared
+on sampled layers, KV heads and query rows.
+"""
+
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_20397_amd import nexus as N
+from synth import gen as G
+
+from _pipeline import (BF16_MAX_ABS, BF16_REL_RMS, F32_TOL, compare, custom_workload,
+                       device_case, gpu_attention, gpu_build_cache, host_subset, oracle_attention,
+                       oracle_cache, to_f64)
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(got, ref, dtype, tag):
+    ma, rr = compare(got, ref)
+    print(f"{tag}: max-abs {ma:.3e} rel-RMS {rr:.3e}", flush=True)
+    assert np.isfinite(got).all(), tag
+    if dtype == "bf16":
+        assert ma <= BF16_MAX_ABS and rr <= BF16_REL_RMS, (tag, ma, rr)
+    else:
+        assert ma <= F32_TOL and rr <= F32_TOL, (tag, ma, rr)
+
+
+def _heads(wl, kv_heads):
+    G_ = wl.group
+    return [h for g in kv_heads for h in range(g * G_, (g + 1) * G_)]
+
+
+def _run_full(hc, tag, **kw):
+    cache = gpu_build_cache(hc, **kw)
+    run = gpu_attention(hc, cache)
+    torch.cuda.synchronize()
+    ck, cv = oracle_cache(hc, **kw)
+    for layer in range(hc.ctx_k.shape[0]):
+        ref = oracle_attention(hc, ck, cv, layer)
+        _check(to_f64(run.out[layer]), ref, hc.wl.dtype, f"{tag} layer {layer}")
+    return run
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 5])
+def test_config_parity(cfg):
+    _run_full(G.host_case(cfg), f"cfg{cfg}")
+
+
+def test_config1_anchored_run():
+    hc = G.host_case(1)
+    hc.wl = dataclasses.replace(hc.wl, anchor=128)   # compiled at 128, spliced at 128
+    _run_full(hc, "cfg1 delta 0")
+
+
+def test_config4_varlen_full_size_sampled():
+    """16 blocks in a shuffled 32k cache, one varlen launch; oracle on sampled blocks/heads."""
+    hc = G.host_case(4)
+    wl = hc.wl
+    cache = gpu_build_cache(hc)
+    run = gpu_attention(hc, cache, varlen=True)
+    torch.cuda.synchronize()
+    ck, cv = oracle_cache(hc)
+    out = to_f64(run.out[0])
+    for b, kvh in [(0, [0, 7]), (9, [3]), (15, [5, 6])]:
+        ref = oracle_attention(hc, ck, cv, 0, block=b, kv_heads=kvh)
+        got = out[b * wl.n_suffix:(b + 1) * wl.n_suffix][:, _heads(wl, kvh)]
+        _check(got, ref, "bf16", f"cfg4 block {b} kv {kvh}")
+
+
+def test_config4_varlen_equals_per_block_calls():
+    hc = G.host_case(4)
+    cache = gpu_build_cache(hc)
+    a = gpu_attention(hc, cache, varlen=True).out[0]
+    b = gpu_attention(hc, cache, varlen=False).out[0]
+    torch.cuda.synchronize()
+    ma, rr = compare(to_f64(a), to_f64(b))
+    assert ma <= BF16_MAX_ABS and rr <= BF16_REL_RMS, (ma, rr)
+
+
+def test_config3_full_size_sampled():
+    """48 layers back to back at full size (device-drawn inputs); oracle on sampled slices."""
+    dc = device_case(3)
+    layers = [0, 23, 47]
+    hc = host_subset(dc, layers)        # host copies of the inputs, taken before any kernel
+    cache = gpu_build_cache(dc)
+    run = gpu_attention(dc, cache)
+    torch.cuda.synchronize()
+    ck, cv = oracle_cache(hc)
+    wl = hc.wl
+    for li, layer in enumerate(layers):
+        out = to_f64(run.out[layer])
+        for kvh, rows in [([0], (0, 40)), ([4], (517, 600)), ([7], (1040, 1088))]:
+            ref = oracle_attention(hc, ck, cv, li, kv_heads=kvh, rows=rows)
+            got = out[rows[0]:rows[1]][:, _heads(wl, kvh)]
+            _check(got, ref, "bf16", f"cfg3 layer {layer} kv {kvh} rows {rows}")
+
+
+# ------------------------------------------------------------------ edge cases
+EDGE = {
+    "single query": dict(base_cfg=2, n_ctx=300, block_len=40, n_user=0, n_suffix=1),
+    "ragged 33 queries": dict(base_cfg=2, n_ctx=1000, block_len=100, n_user=7, n_suffix=33),
+    "no past (n_past 0)": dict(base_cfg=2, n_ctx=0, block_len=50, n_user=0, n_suffix=50),
+    "cache full to capacity": dict(base_cfg=2, n_ctx=3000, block_len=1000, n_user=96, n_suffix=200),
+    "GQA group 1": dict(base_cfg=2, n_ctx=700, block_len=64, n_user=0, n_suffix=64, n_q_heads=8),
+    "head_dim 64": dict(base_cfg=2, n_ctx=900, block_len=128, n_user=3, n_suffix=100,
+                        head_dim=64, n_q_heads=16, n_kv_heads=4),
+    "head_dim 256 row-major V": dict(base_cfg=5, n_ctx=1500, block_len=256, n_user=0,
+                                     n_suffix=96, v_layout="rowmajor"),
+    "saturating soft-cap": dict(base_cfg=5, n_ctx=1200, block_len=256, n_user=0, n_suffix=128,
+                                softcap=5.0),
+    "transposed V shuffled pages": dict(base_cfg=5, n_ctx=777, block_len=300, n_user=5,
+                                        n_suffix=130, shuffled_pages=True),
+    "unscaled N(0,1): peaked softmax": dict(base_cfg=2, n_ctx=1500, block_len=256, n_user=0,
+                                            n_suffix=100, q_scale=1.0, k_scale=1.0, v_scale=1.0),
+    "many splits": dict(base_cfg=2, n_ctx=20000, block_len=16, n_user=0, n_suffix=8,
+                        n_q_heads=40),
+    "fp32 transposed V G=2": dict(base_cfg=1, n_ctx=500, block_len=64, n_user=10, n_suffix=40,
+                                  n_q_heads=4, n_kv_heads=2, v_layout="transposed", softcap=3.0),
+}
+
+
+@pytest.mark.parametrize("name", list(EDGE))
+def test_edge_case(name):
+    kw = dict(EDGE[name])
+    base = kw.pop("base_cfg")
+    wl = custom_workload(base, **kw)
+    hc = G.host_case_wl(wl, 100 + list(EDGE).index(name))
+    _run_full(hc, name)
+
+
+def test_rerun_and_page_table_invariance():
+    """Reruns are bit-identical; identity vs shuffled physical pages give identical bits."""
+    hc = G.host_case(2)
+    cache_a = gpu_build_cache(hc)
+    rng = np.random.default_rng(5)
+    perm = rng.permutation(hc.wl.n_pages + 9)[:hc.wl.n_pages].astype(np.int32)
+    cache_b = gpu_build_cache(hc, n_phys_pages=hc.wl.n_pages + 9, page_map=perm)
+    o1 = gpu_attention(hc, cache_a).out[0]
+    o2 = gpu_attention(hc, cache_a).out[0]
+    o3 = gpu_attention(hc, cache_b).out[0]
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(o1.view(torch.int16), o3.view(torch.int16))
+
+
+def test_transposed_equals_rowmajor_values():
+    """The same logical V in both layouts gives outputs within tolerance of each other."""
+    wl_t = custom_workload(5, n_ctx=1000, block_len=200, n_user=0, n_suffix=100)
+    wl_r = dataclasses.replace(wl_t, v_layout="rowmajor")
+    hc_t = G.host_case_wl(wl_t, 77)
+    hc_r = G.host_case_wl(wl_r, 77)
+    a = gpu_attention(hc_t, gpu_build_cache(hc_t)).out[0]
+    b = gpu_attention(hc_r, gpu_build_cache(hc_r)).out[0]
+    torch.cuda.synchronize()
+    ma, rr = compare(to_f64(a), to_f64(b))
+    assert ma <= BF16_MAX_ABS and rr <= BF16_REL_RMS, (ma, rr)
+
+
+def test_attention_rejects_layout_mismatch():
+    hc = G.host_case(5)
+    cache = gpu_build_cache(hc)
+    q = G.bits_to_torch(hc.q[0], "bf16", "cuda")
+    with pytest.raises(N.NexusError) as e:
+        N.suffix_attn(q, cache, 0, hc.wl.attn_n_past[0], hc.wl.softcap, v_layout=N.V_ROWMAJOR)
+    assert e.value.status == N.ELAYOUT

@@ -1,0 +1,165 @@
+"""GPU parity of the splice and re-anchor kernels against the oracle (bit level).
+
+* Splice: every cache element must equal the oracle's bits (pure data movement), including the
+  NaN sentinel in every slot the splice must not touch.
+* Re-anchor: the rotated key rows must lie within 1 bf16 ulp of the oracle's fp64 rotation
+  rounded to nearest-even (at least 99.9% exactly equal), or within 1e-5 for f32 keys; every
+  other element keeps its bits; delta 0 is bit-exact.
+"""
+
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2608_20397_amd import nexus as N
+from synth import PAGE
+from synth import gen as G
+
+from _pipeline import VL, gpu_build_cache, oracle_cache
+
+pytestmark = pytest.mark.gpu
+
+
+def _range_mask(wl, L, n_phys_pages, page_map):
+    """Boolean K-cache mask of the re-anchored block rows, by oracle addressing."""
+    shape = (L, n_phys_pages, wl.n_kv_heads, PAGE, wl.head_dim)
+    m = np.zeros(shape, bool)
+    for pos in wl.splice_pos:
+        for t in range(pos, pos + wl.block_len):
+            m[:, page_map[t // PAGE], :, t % PAGE, :] = True
+    return m
+
+
+def _check_keys(gk, ok, mask, dtype, tag):
+    assert np.array_equal(gk[~mask], ok[~mask]), f"{tag}: bits outside the re-anchored rows"
+    if dtype == "bf16":
+        a = O.bf16_bits_to_f64(gk[mask])
+        b = O.bf16_bits_to_f64(ok[mask])
+        ulp = np.abs(b) * 2.0 ** -7
+        ulp = np.maximum(ulp, 2.0 ** -133)
+        assert np.all(np.abs(a - b) <= ulp + 1e-300), f"{tag}: more than 1 ulp"
+        exact = np.mean(gk[mask] == ok[mask])
+        assert exact >= 0.999, f"{tag}: only {exact:.5f} exactly rounded"
+    else:
+        a = gk[mask].view(np.float32).astype(np.float64)
+        b = ok[mask].view(np.float32).astype(np.float64)
+        assert np.max(np.abs(a - b)) <= 1e-5, f"{tag}: f32 keys off by {np.max(np.abs(a - b))}"
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 4, 5])
+def test_splice_rephase_cache_parity(cfg):
+    hc = G.host_case(cfg)
+    wl = hc.wl
+    extra = 3                                   # physical pages no logical page maps to
+    npp = wl.n_pages + extra
+    cache = gpu_build_cache(hc, n_phys_pages=npp)
+    torch.cuda.synchronize()
+    ck, cv = oracle_cache(hc, n_phys_pages=npp)
+    gk, gv = G.torch_to_bits(cache.k), G.torch_to_bits(cache.v)
+    assert np.array_equal(gv, cv), "V cache bits differ"
+    mask = _range_mask(wl, 1, npp, hc.page_map)
+    _check_keys(gk, ck, mask, wl.dtype, f"cfg{cfg}")
+    # the unmapped physical pages still hold the sentinel
+    s = G.SENTINEL[wl.dtype]
+    unmapped = sorted(set(range(npp)) - set(hc.page_map.tolist()))
+    assert len(unmapped) == extra
+    assert (gk[:, unmapped] == s).all()
+
+
+def test_anchored_splice_is_bit_exact():
+    """Config 1, second run: a block compiled at 128 spliced at 128 (delta 0) is bit-exact."""
+    hc = G.host_case(1)
+    hc.wl = dataclasses.replace(hc.wl, anchor=128)
+    cache = gpu_build_cache(hc)
+    torch.cuda.synchronize()
+    ck, cv = oracle_cache(hc)
+    assert np.array_equal(G.torch_to_bits(cache.k), ck)
+    assert np.array_equal(G.torch_to_bits(cache.v), cv)
+    lk, _ = O.gather_logical(G.torch_to_bits(cache.k), G.torch_to_bits(cache.v), hc.page_map, 224,
+                             PAGE)
+    assert np.array_equal(lk[:, 128:192], hc.blk_k[0])
+
+
+@pytest.mark.parametrize("dtype,style,D,base", [("bf16", N.ROPE_NEOX, 128, 1e6),
+                                                ("bf16", N.ROPE_INTERLEAVED, 128, 1e6),
+                                                ("bf16", N.ROPE_NEOX, 256, 1e4),
+                                                ("f32", N.ROPE_NEOX, 64, 1e4),
+                                                ("f32", N.ROPE_INTERLEAVED, 64, 1e4)])
+def test_rephase_block_contiguous(dtype, style, D, base):
+    rng = np.random.default_rng(D + style)
+    L, T, H = 3, 77, 2
+    bits = G.to_bits(rng.standard_normal((L, T, H, D)), dtype)
+    k = G.bits_to_torch(bits, dtype, "cuda")
+    v = k.clone()
+    v_bits = bits.copy()
+    blk = N.Block(k, v, base_pos=5, rope_base=base, rope_style=style)
+    N.rephase_k(blk, 5, 5, base)                   # delta 0: identity, nothing enqueued
+    torch.cuda.synchronize()
+    assert np.array_equal(G.torch_to_bits(k), bits)
+    st = O.NEOX if style == N.ROPE_NEOX else O.INTERLEAVED
+    ref = bits
+    for dst in (32767, 4101):                      # two re-anchors in a row, oracle chained alike
+        src = blk.base_pos
+        N.rephase_k(blk, src, dst, base)
+        torch.cuda.synchronize()
+        assert blk.base_pos == dst
+        ref = O.round_to_storage(O.rephase(O.storage_to_f64(ref, dtype), src, dst, base, st), dtype)
+        if dst == 32767:
+            _check_keys(G.torch_to_bits(k), ref, np.ones(bits.shape, bool), dtype, f"{dtype} {style}")
+    # after two roundings the chains may part by the first step's rare 1-ulp differences
+    got = O.storage_to_f64(G.torch_to_bits(k), dtype)
+    want = O.storage_to_f64(ref, dtype)
+    assert np.max(np.abs(got - want)) <= (2.0 ** -6 * np.abs(want).max() if dtype == "bf16" else 2e-5)
+    assert np.array_equal(G.torch_to_bits(v), v_bits)                # V is never rotated
+    with pytest.raises(N.NexusError):
+        N.rephase_k(blk, 0, 10, base)              # wrong anchor: fail closed
+
+
+def test_rephase_leaves_values_untouched():
+    rng = np.random.default_rng(1)
+    bits = G.to_bits(rng.standard_normal((1, 40, 2, 128)), "bf16")
+    k = G.bits_to_torch(bits, "bf16", "cuda")
+    v = G.bits_to_torch(bits, "bf16", "cuda")
+    N.rephase_k(N.Block(k, v, 0, 1e6), 0, 999, 1e6)
+    torch.cuda.synchronize()
+    assert np.array_equal(G.torch_to_bits(v), bits)
+    assert not np.array_equal(G.torch_to_bits(k), bits)
+
+
+@pytest.mark.parametrize("v_layout", ["rowmajor", "transposed"])
+@pytest.mark.parametrize("offset,T", [(0, 16), (5, 1), (7, 50), (37, 200), (1, 255)])
+def test_unaligned_splice_edges(v_layout, offset, T):
+    """Blocks that start and end inside pages share those pages with untouched slots."""
+    wl = dataclasses.replace(G.get_workload(2), n_tokens=512, block_len=T, splice_pos=(offset,),
+                             n_user=0, v_layout=v_layout, shuffled_pages=True, n_layers=2)
+    rng = np.random.default_rng(offset * 1000 + T)
+    blk_k = G.to_bits(rng.standard_normal((2, T, 8, 128)), "bf16")
+    blk_v = G.to_bits(rng.standard_normal((2, T, 8, 128)), "bf16")
+    pm = rng.permutation(wl.n_pages + 4)[:wl.n_pages].astype(np.int32)
+    npp = wl.n_pages + 4
+    kb, vb = G.empty_cache_bits(wl, 2, npp)
+    cache = N.PagedKVCache(G.bits_to_torch(kb, "bf16", "cuda"), G.bits_to_torch(vb, "bf16", "cuda"),
+                           torch.from_numpy(pm).cuda(), wl.rope_base, VL[v_layout])
+    N.splice_pages(cache, N.Block(G.bits_to_torch(blk_k, "bf16", "cuda"),
+                                  G.bits_to_torch(blk_v, "bf16", "cuda"), 0, wl.rope_base), offset)
+    torch.cuda.synchronize()
+    ok, ov = O.splice_paged(kb, vb, pm, blk_k, blk_v, offset, PAGE, v_layout)
+    assert np.array_equal(G.torch_to_bits(cache.k), ok)
+    assert np.array_equal(G.torch_to_bits(cache.v), ov)
+
+
+def test_splice_rejects_mismatched_header():
+    wl = G.get_workload(2)
+    kb, vb = G.empty_cache_bits(wl, 1)
+    cache = N.PagedKVCache(G.bits_to_torch(kb, "bf16", "cuda"), G.bits_to_torch(vb, "bf16", "cuda"),
+                           torch.arange(wl.n_pages, dtype=torch.int32, device="cuda"), 1e6)
+    k = torch.zeros(1, 16, 8, 128, dtype=torch.bfloat16, device="cuda")
+    before = G.torch_to_bits(cache.k)
+    with pytest.raises(N.NexusError) as e:
+        N.splice_pages(cache, N.Block(k, k.clone(), 0, 1e4), 0)     # block compiled with base 1e4
+    assert e.value.status == N.EROPE
+    torch.cuda.synchronize()
+    assert np.array_equal(G.torch_to_bits(cache.k), before)

@@ -378,3 +378,20 @@ def test_layout_and_page_table_invariance():
             res.append(O.suffix_attention(q, O.bf16_bits_to_f64(lk[0]), O.bf16_bits_to_f64(lv[0]), n - 10))
     for r in res[1:]:
         assert np.array_equal(r, res[0])
+
+
+def test_rephase_paged_bits_rounds_only_the_range():
+    """Bit-level re-anchor: the range equals the rounded fp64 rotation; all else keeps its bits."""
+    rng = np.random.default_rng(12)
+    L, npg, H, P, D = 2, 5, 2, 16, 32
+    ck = np.full((L, npg, H, P, D), 0x7FC1, np.uint16)                # NaN sentinel
+    perm = rng.permutation(npg).astype(np.int32)
+    blk = O.f64_to_bf16_bits(rng.standard_normal((L, 30, H, D)))
+    ck, _ = O.splice_paged(ck, ck.copy(), perm, blk, blk, 21, P)
+    out = O.rephase_paged_bits(ck, "bf16", perm, P, 21, 30, 0, 999, 1e4)
+    lk, _ = O.gather_logical(out, out, perm, npg * P, P)
+    ref = O.f64_to_bf16_bits(O.rephase(O.bf16_bits_to_f64(blk), 0, 999, 1e4))
+    assert np.array_equal(lk[:, 21:51], ref)
+    l0, _ = O.gather_logical(ck, ck, perm, npg * P, P)
+    assert np.array_equal(lk[:, :21], l0[:, :21]) and np.array_equal(lk[:, 51:], l0[:, 51:])
+    assert np.array_equal(O.rephase_paged_bits(ck, "bf16", perm, P, 21, 30, 5, 5, 1e4), ck)
