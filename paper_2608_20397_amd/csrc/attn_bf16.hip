@@ -31,6 +31,7 @@ namespace nexus {
 constexpr int kMaxSeqs = 32;
 constexpr int kWaves = 4;
 constexpr int kQB = 32;   // queries per wave task
+constexpr int kMaxSplitKeys = 16384;   // keys one workgroup covers at most
 
 struct SeqPlan {
   int32_t q_start;     // first row of q / out
@@ -83,8 +84,15 @@ __device__ __forceinline__ int vt_pos(int k) {
 
 }  // namespace
 
+// V^T tile row swizzle: 16-byte chunk c of feature row d lives at chunk c ^ vt_swz(d).  Distinct
+// for 8 consecutive rows (conflict-free operand reads) and for rows 8 apart (tile writes).
+template <int VSW>
+__device__ __forceinline__ int vt_swz(int d) {
+  return (d ^ (d >> 3)) & VSW;
+}
+
 template <int D, int KT, bool VT, bool CAP>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const AttnPlan plan) {
+__global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(const AttnArgs a, const AttnPlan plan) {
   constexpr int KCH = D / 8;                        // 16-byte chunks per K row
   constexpr int KSW = (KCH < 16 ? KCH : 16) - 1;    // K row swizzle mask
   constexpr int VCH = KT / 8;                       // 16-byte chunks per V^T row
@@ -92,8 +100,9 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const 
   constexpr int NKB = KT / 32;                      // 32-key score blocks per tile
   constexpr int NDB = D / 32;                       // 32-row blocks of O^T
   constexpr int NS = D / 16;                        // k-steps of Q K^T
-  __shared__ __align__(16) uint16_t Ks[KT * D];
-  __shared__ __align__(16) uint16_t Vs[D * KT];
+  __shared__ __align__(16) uint16_t Ks[2][KT * D];
+  __shared__ __align__(16) uint16_t Vs[2][D * KT];
+  __shared__ int32_t pg[kMaxSplitKeys / kPage + 1];  // physical pages of this workgroup's keys
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -116,11 +125,20 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const 
   const int qhead = kvh * G + g;
   const int last_task = min(tgrp * kWaves + kWaves - 1, sp.n_tasks - 1);
   const int last_q = min((last_task / G + 1) * kQB, sp.len);
-  const int64_t wg_keys = sp.n_past + last_q;
-  const int64_t k_begin = (int64_t)split * sp.split_keys;
-  const int64_t k_end = min(k_begin + (int64_t)sp.split_keys, wg_keys);
-  const int64_t wave_keys = active ? sp.n_past + min(q0 + kQB, sp.len) : 0;
-  const int64_t qpos0 = sp.n_past + q0;  // position of this wave's query 0
+  // positions fit in int32 (the host checks the cache capacity)
+  const int wg_keys = (int)sp.n_past + last_q;
+  const int k_begin = split * sp.split_keys;
+  const int k_end = min(k_begin + sp.split_keys, wg_keys);
+  const int wave_keys = active ? (int)sp.n_past + min(q0 + kQB, sp.len) : 0;
+  const int qpos0 = (int)sp.n_past + q0;  // position of this wave's query 0
+  const int n_tiles = k_end > k_begin ? (k_end - k_begin + KT - 1) / KT : 0;
+
+  // physical page of every logical page this workgroup reads
+  const int pg0 = k_begin >> kPageShift;
+  if (n_tiles > 0) {
+    const int n_pg = ((k_end - 1) >> kPageShift) - pg0 + 1;
+    for (int i = tid; i < n_pg; i += 256) pg[i] = a.map[pg0 + i];
+  }
 
   // Q of this wave as B operands: lane (hh, j) holds Q[q0 + j][16 s + 8 hh .. + 7].
   bf16x8 qreg[NS];
@@ -141,6 +159,8 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const 
 
   const int64_t hstride = (int64_t)kPage * D;               // one (page, head) slab
   const int64_t n_cols = (int64_t)a.n_phys_pages * kPage;   // transposed V row length
+  const uint16_t *kbase = a.kc + (int64_t)kvh * hstride;
+  const int64_t pstride = (int64_t)a.n_kv_heads * hstride;   // one physical page, all heads
 
   // ---- global -> register staging of one tile
   constexpr int K_ITEMS = KT * KCH / 256;                   // 16-byte K chunks per thread
@@ -152,21 +172,25 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const 
   uint4 kreg[K_ITEMS];
   uint4 vreg[VT ? V_PER_T_T : 4 * V_PER_T_RM];
 
-  auto load_tile = [&](int64_t kt) {
+  __syncthreads();   // pg[] visible
+
+  auto page_of = [&](int t) -> int64_t { return pg[(t >> kPageShift) - pg0]; };
+
+  auto load_tile = [&](int kt) {
 #pragma unroll
     for (int i = 0; i < K_ITEMS; ++i) {
       const int u = tid + 256 * i;
       const int key = u / KCH, c = u % KCH;
-      const int64_t t = kt + key;
+      const int t = kt + key;
       if (t < k_end) {
-        const int64_t page = a.map[t >> kPageShift];
-        kreg[i] = *reinterpret_cast<const uint4 *>(
-            a.kc + (page * a.n_kv_heads + kvh) * hstride + (t & (kPage - 1)) * D + c * 8);
+        kreg[i] = *reinterpret_cast<const uint4 *>(kbase + page_of(t) * pstride +
+                                                   (t & (kPage - 1)) * D + c * 8);
       } else {
         kreg[i] = make_uint4(0, 0, 0, 0);
       }
     }
     if constexpr (!VT) {
+      const uint16_t *vbase = a.vc + (int64_t)kvh * hstride;
 #pragma unroll
       for (int i = 0; i < V_PER_T_RM; ++i) {
         const int u = tid + 256 * i;
@@ -175,12 +199,10 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const 
           uint4 val = make_uint4(0, 0, 0, 0);
           if (u < V_ITEMS_RM) {
             const int tg4 = u / (D / 8), dc = u % (D / 8);
-            const int64_t t = kt + 4 * tg4 + e;
-            if (t < k_end) {
-              const int64_t page = a.map[t >> kPageShift];
-              val = *reinterpret_cast<const uint4 *>(
-                  a.vc + (page * a.n_kv_heads + kvh) * hstride + (t & (kPage - 1)) * D + dc * 8);
-            }
+            const int t = kt + 4 * tg4 + e;
+            if (t < k_end)
+              val = *reinterpret_cast<const uint4 *>(vbase + page_of(t) * pstride +
+                                                     (t & (kPage - 1)) * D + dc * 8);
           }
           vreg[4 * i + e] = val;
         }
@@ -191,31 +213,32 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const 
       for (int i = 0; i < V_PER_T_T; ++i) {
         const int u = tid + 256 * i;
         const int d = u / (KT / 8), grp = u % (KT / 8);
-        const int64_t t0 = kt + 8 * grp;
+        const int t0 = kt + 8 * grp;
         uint4 val = make_uint4(0, 0, 0, 0);
-        if (t0 + 8 <= k_end) {
-          const int64_t page = a.map[t0 >> kPageShift];
-          val = *reinterpret_cast<const uint4 *>(vrow0 + (int64_t)d * n_cols + page * kPage +
-                                                 (t0 & (kPage - 1)));
-        } else if (t0 < k_end) {
-          const int64_t page = a.map[t0 >> kPageShift];
-          const uint16_t *src = vrow0 + (int64_t)d * n_cols + page * kPage + (t0 & (kPage - 1));
-          uint32_t w[4] = {0, 0, 0, 0};
-          for (int e = 0; e < 8; ++e)
-            if (t0 + e < k_end) w[e >> 1] |= (uint32_t)src[e] << (16 * (e & 1));
-          val = make_uint4(w[0], w[1], w[2], w[3]);
+        if (t0 < k_end) {
+          const uint16_t *src = vrow0 + (int64_t)d * n_cols + page_of(t0) * kPage + (t0 & (kPage - 1));
+          if (t0 + 8 <= k_end) {
+            val = *reinterpret_cast<const uint4 *>(src);
+          } else {
+            uint32_t w[4] = {0, 0, 0, 0};
+            for (int e = 0; e < 8; ++e)
+              if (t0 + e < k_end) w[e >> 1] |= (uint32_t)src[e] << (16 * (e & 1));
+            val = make_uint4(w[0], w[1], w[2], w[3]);
+          }
         }
         vreg[i] = val;
       }
     }
   };
 
-  auto store_tile = [&]() {
+  auto store_tile = [&](int buf) {
+    uint16_t *ks = Ks[buf];
+    uint16_t *vs = Vs[buf];
 #pragma unroll
     for (int i = 0; i < K_ITEMS; ++i) {
       const int u = tid + 256 * i;
       const int key = u / KCH, c = u % KCH;
-      *reinterpret_cast<uint4 *>(Ks + key * D + ((c ^ (key & KSW)) * 8)) = kreg[i];
+      *reinterpret_cast<uint4 *>(ks + key * D + ((c ^ (key & KSW)) * 8)) = kreg[i];
     }
     if constexpr (!VT) {
 #pragma unroll
@@ -241,7 +264,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const 
               hi = (w2[wi] & 0xFFFFu) | (w3[wi] << 16);
             }
             const int d = 8 * dc + dd;
-            *reinterpret_cast<uint2 *>(Vs + d * KT + ((cc ^ (d & VSW)) * 8) + half * 4) =
+            *reinterpret_cast<uint2 *>(vs + d * KT + ((cc ^ vt_swz<VSW>(d)) * 8) + half * 4) =
                 make_uint2(lo, hi);
           }
         }
@@ -257,95 +280,103 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a, const 
           const int pos = (k4 & ~15) | vt_pos(k4 & 15);
           const int cc = pos >> 3, half = (pos >> 2) & 1;
           const uint2 piece = hf ? make_uint2(vreg[i].z, vreg[i].w) : make_uint2(vreg[i].x, vreg[i].y);
-          *reinterpret_cast<uint2 *>(Vs + d * KT + ((cc ^ (d & VSW)) * 8) + half * 4) = piece;
+          *reinterpret_cast<uint2 *>(vs + d * KT + ((cc ^ vt_swz<VSW>(d)) * 8) + half * 4) = piece;
         }
       }
     }
   };
 
-  if (k_begin < k_end) load_tile(k_begin);
-  for (int64_t kt = k_begin; kt < k_end; kt += KT) {
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    if (kt + KT < k_end) load_tile(kt + KT);
-    if (!active || kt >= wave_keys) continue;
-
-    // ---- S^T = K . Q^T
-    f32x16 sacc[NKB];
+  // ---- pipeline: tile t is in LDS buffer t & 1 while tile t + 1 waits in registers
+  if (n_tiles > 0) {
+    load_tile(k_begin);
+    store_tile(0);
+    if (n_tiles > 1) load_tile(k_begin + KT);
+  }
+  __syncthreads();
+  for (int it = 0; it < n_tiles; ++it) {
+    const int kt = k_begin + it * KT;
+    const uint16_t *ks = Ks[it & 1];
+    const uint16_t *vs = Vs[it & 1];
+    if (active && kt < wave_keys) {
+      // ---- S^T = K . Q^T
+      f32x16 sacc[NKB];
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) {
+      for (int kb = 0; kb < NKB; ++kb) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) sacc[kb][v] = 0.f;
-      const int key = 32 * kb + j;
+        for (int v = 0; v < 16; ++v) sacc[kb][v] = 0.f;
+        const int key = 32 * kb + j;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const bf16x8 ka =
-            *reinterpret_cast<const bf16x8 *>(Ks + key * D + (((2 * s + hh) ^ (key & KSW)) * 8));
-        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[s], sacc[kb], 0, 0, 0);
+        for (int s = 0; s < NS; ++s) {
+          const bf16x8 ka =
+              *reinterpret_cast<const bf16x8 *>(ks + key * D + (((2 * s + hh) ^ (key & KSW)) * 8));
+          sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[s], sacc[kb], 0, 0, 0);
+        }
       }
+
+      // ---- scores in log2 units, masking, online softmax
+      const bool need_mask = (kt + KT > k_end) || (kt + KT - 1 > qpos0);
+      const int my_pos = qpos0 + j;
+      float mt = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          float x;
+          if constexpr (CAP) x = a.cap_out * tanh_fast(sacc[kb][v] * a.cap_in);
+          else x = sacc[kb][v] * a.scale_log2;
+          if (need_mask) {
+            const int key = kt + 32 * kb + 8 * (v >> 2) + 4 * hh + (v & 3);
+            if (key >= k_end || key > my_pos) x = -INFINITY;
+          }
+          sacc[kb][v] = x;
+          mt = fmaxf(mt, x);
+        }
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      const float m_new = fmaxf(m, mt);
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      const float alpha = fast_exp2(m - m_use);
+      float psum = 0.f;
+      bf16x8 pb[NKB][2];
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          float p[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            p[e] = fast_exp2(sacc[kb][8 * hf + e] - m_use);
+            psum += p[e];
+          }
+          uint32_t w[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(p[2 * e], p[2 * e + 1]);
+          pb[kb][hf] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
+        }
+      l = l * alpha + psum;
+      m = m_new;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+
+      // ---- O^T += V^T . P^T
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int ks2 = 2 * kb + hf;
+#pragma unroll
+          for (int db = 0; db < NDB; ++db) {
+            const int d = 32 * db + j;
+            const bf16x8 va = *reinterpret_cast<const bf16x8 *>(
+                vs + d * KT + (((2 * ks2 + hh) ^ vt_swz<VSW>(d)) * 8));
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kb][hf], o[db], 0, 0, 0);
+          }
+        }
     }
-
-    // ---- scores in log2 units, masking, online softmax
-    const bool need_mask = (kt + KT > k_end) || (kt + KT - 1 > qpos0);
-    const int64_t my_pos = qpos0 + j;
-    float mt = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        float x;
-        if constexpr (CAP) x = a.cap_out * tanh_fast(sacc[kb][v] * a.cap_in);
-        else x = sacc[kb][v] * a.scale_log2;
-        if (need_mask) {
-          const int64_t key = kt + 32 * kb + 8 * (v >> 2) + 4 * hh + (v & 3);
-          if (key >= k_end || key > my_pos) x = -INFINITY;
-        }
-        sacc[kb][v] = x;
-        mt = fmaxf(mt, x);
-      }
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m, mt);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = fast_exp2(m - m_use);
-    float psum = 0.f;
-    bf16x8 pb[NKB][2];
-#pragma unroll
-    for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        float p[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          p[e] = fast_exp2(sacc[kb][8 * hf + e] - m_use);
-          psum += p[e];
-        }
-        uint32_t w[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(p[2 * e], p[2 * e + 1]);
-        pb[kb][hf] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
-      }
-    l = l * alpha + psum;
-    m = m_new;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
-
-    // ---- O^T += V^T . P^T
-#pragma unroll
-    for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        const int ks = 2 * kb + hf;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const int d = 32 * db + j;
-          const bf16x8 va = *reinterpret_cast<const bf16x8 *>(
-              Vs + d * KT + (((2 * ks + hh) ^ (d & VSW)) * 8));
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kb][hf], o[db], 0, 0, 0);
-        }
-      }
+    if (it + 1 < n_tiles) store_tile((it + 1) & 1);
+    if (it + 2 < n_tiles) load_tile(kt + 2 * KT);
+    __syncthreads();
   }
 
   // ---- epilogue
@@ -452,7 +483,8 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   }
   const double per_wg = key_work * p.n_kv_heads / target_workgroups();
   int64_t split_keys = (int64_t)per_wg;
-  if (split_keys < 1024) split_keys = 1024;
+  if (split_keys < 512) split_keys = 512;
+  if (split_keys > kMaxSplitKeys) split_keys = kMaxSplitKeys;
   split_keys = (split_keys + KT - 1) / KT * KT;
   int32_t unit = 0, rows = 0;
   int64_t ws_floats = 0;

@@ -2,10 +2,11 @@
 // by delta * theta_i, theta_i = base^(-2i/D), delta = splice position - compile anchor
 // (the inverse of the drift of eq. (drift)).  In place; V is never touched.
 //
-// HBM-bound: each thread owns a fixed group of feature pairs, forms their angles once in fp64
-// (reduced modulo 2*pi in fp64, cosine and sine in fp64 rounded to fp32), keeps cos/sin in
-// registers, and then streams rows with 16-byte loads and stores.  bf16 keys rotate in fp32 and
-// round to nearest-even; f32 keys rotate in fp64 and round once.
+// HBM-bound: each workgroup forms the D/2 angles once in fp64 (reduced modulo 2*pi in fp64) and
+// keeps their cosine and sine (fp64) in LDS; each thread owns a fixed group of feature pairs,
+// holds their cos/sin in registers and streams rows with 16-byte loads and stores.  The rotation
+// runs in fp64 and is rounded once to the storage type (nearest-even), so near-zero results do
+// not suffer fp32 cancellation.
 #include "device_common.h"
 #include "launch.h"
 
@@ -15,6 +16,7 @@ namespace {
 
 constexpr double kTwoPiHi = 6.283185307179586232;       // fp64(2*pi)
 constexpr double kTwoPiLo = 2.4492935982947064e-16;     // 2*pi - fp64(2*pi)
+constexpr int kMaxPairs = 512;                            // head_dim <= 1024
 
 __device__ __forceinline__ void pair_angle(int64_t delta, double base, int i, int head_dim,
                                            double &c, double &s) {
@@ -40,6 +42,12 @@ struct Pack<uint16_t> {  // 8 bf16
       x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
     }
   }
+  // fp64 -> bf16 with one rounding: round-to-odd into fp32 (24 >= 8 + 2 bits), then the
+  // nearest-even fp32 -> bf16 conversion.
+  __device__ static float to_odd(double x) {
+    const float f = __double2float_rz(x);
+    return ((double)f == x) ? f : __uint_as_float(__float_as_uint(f) | 1u);
+  }
   __device__ static uint4 pack(const float *x) {
     uint4 v;
     v.x = pack_bf16x2(x[0], x[1]);
@@ -53,6 +61,7 @@ struct Pack<uint16_t> {  // 8 bf16
 template <>
 struct Pack<uint32_t> {  // 4 f32
   static constexpr int N = 4;
+  __device__ static float to_odd(double x) { return (float)x; }  // f32 keys: one RNE rounding
   __device__ static void unpack(const uint4 &v, float *x) {
     x[0] = __uint_as_float(v.x);
     x[1] = __uint_as_float(v.y);
@@ -65,22 +74,14 @@ struct Pack<uint32_t> {  // 4 f32
   }
 };
 
-// Rotate pairs (a[e], b[e]) by (c[e], s[e]).
-template <typename T>
-__device__ __forceinline__ void rotate(float *a, float *b, const float *c, const float *s,
-                                       const double *cd, const double *sd) {
-  constexpr int N = Pack<T>::N;
+// Rotate pairs (a[e], b[e]) by (c[e], s[e]) in fp64.
+template <typename P, int N>
+__device__ __forceinline__ void rotate(float *a, float *b, const double *c, const double *s) {
 #pragma unroll
   for (int e = 0; e < N; ++e) {
-    if constexpr (sizeof(T) == 2) {
-      const float xa = a[e], xb = b[e];
-      a[e] = xa * c[e] - xb * s[e];
-      b[e] = xa * s[e] + xb * c[e];
-    } else {
-      const double xa = a[e], xb = b[e];
-      a[e] = (float)(xa * cd[e] - xb * sd[e]);
-      b[e] = (float)(xa * sd[e] + xb * cd[e]);
-    }
+    const double xa = a[e], xb = b[e];
+    a[e] = P::to_odd(xa * c[e] - xb * s[e]);
+    b[e] = P::to_odd(xa * s[e] + xb * c[e]);
   }
 }
 
@@ -94,18 +95,20 @@ __global__ __launch_bounds__(256) void rephase_kernel(
     uint32_t tpr_shift, FastDiv div_heads, FastDiv div_layer_rows, uint32_t n_heads,
     uint32_t n_tokens, uint32_t n_phys_pages, int32_t head_dim, int64_t delta, double base) {
   constexpr int N = Pack<T>::N;
+  __shared__ double cs_tab[2][kMaxPairs];
+  for (int i = threadIdx.x; i < head_dim / 2; i += blockDim.x)
+    pair_angle(delta, base, i, head_dim, cs_tab[0][i], cs_tab[1][i]);
+  __syncthreads();
+
   const uint32_t tpr = 1u << tpr_shift;  // threads per row
   const uint32_t gtid = blockIdx.x * blockDim.x + threadIdx.x;
   const uint32_t c = gtid & (tpr - 1);
   const uint32_t row_step = (gridDim.x * blockDim.x) >> tpr_shift;
-
-  float cf[N], sf[N];
   double cd[N], sd[N];
 #pragma unroll
   for (int e = 0; e < N; ++e) {
-    pair_angle(delta, base, (int)(N * c + e), head_dim, cd[e], sd[e]);
-    cf[e] = (float)cd[e];
-    sf[e] = (float)sd[e];
+    cd[e] = cs_tab[0][N * c + e];
+    sd[e] = cs_tab[1][N * c + e];
   }
 
   for (uint32_t r = gtid >> tpr_shift; r < n_rows; r += row_step) {
@@ -147,7 +150,7 @@ __global__ __launch_bounds__(256) void rephase_kernel(
         b[e] = x[N + e];
       }
     }
-    rotate<T>(a, b, cf, sf, cd, sd);
+    rotate<Pack<T>, N>(a, b, cd, sd);
     if constexpr (INTERLEAVED) {
 #pragma unroll
       for (int e = 0; e < N; ++e) {
@@ -173,9 +176,10 @@ hipError_t launch_rephase(const RephaseLaunch &p, hipStream_t stream) {
   while ((1u << shift) < tpr) ++shift;
   const uint64_t rows = (uint64_t)p.n_layers * p.n_tokens * p.n_heads;
   const uint64_t threads_needed = rows << shift;
-  uint64_t blocks = (threads_needed + 256 * 4 - 1) / (256 * 4);   // ~4 rows per thread
+  // about 16 rows per thread, at most 2048 workgroups: the per-workgroup angle table is cheap
+  uint64_t blocks = (threads_needed + 256 * 16 - 1) / (256 * 16);
   if (blocks < 1) blocks = 1;
-  if (blocks > 1u << 20) blocks = 1u << 20;
+  if (blocks > 2048) blocks = 2048;
   const FastDiv dh = make_fastdiv((uint32_t)p.n_heads);
   const FastDiv dl = make_fastdiv((uint32_t)(p.n_tokens * p.n_heads));
   if (p.dtype_bytes == 2) {
