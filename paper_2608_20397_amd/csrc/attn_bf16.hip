@@ -92,7 +92,8 @@ __device__ __forceinline__ int vt_swz(int d) {
 }
 
 template <int D, int KT, bool VT, bool CAP>
-__global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(const AttnArgs a, const AttnPlan plan) {
+__global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(const AttnArgs a,
+                                                                             const AttnPlan plan) {
   constexpr int KCH = D / 8;                        // 16-byte chunks per K row
   constexpr int KSW = (KCH < 16 ? KCH : 16) - 1;    // K row swizzle mask
   constexpr int VCH = KT / 8;                       // 16-byte chunks per V^T row
@@ -100,9 +101,11 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
   constexpr int NKB = KT / 32;                      // 32-key score blocks per tile
   constexpr int NDB = D / 32;                       // 32-row blocks of O^T
   constexpr int NS = D / 16;                        // k-steps of Q K^T
+  constexpr int TPG = KT / kPage;                   // pages per tile
+  constexpr float kSlack = 8.0f;                    // lazy rescale: p <= 2^8 between rescales
   __shared__ __align__(16) uint16_t Ks[2][KT * D];
   __shared__ __align__(16) uint16_t Vs[2][D * KT];
-  __shared__ int32_t pg[kMaxSplitKeys / kPage + 1];  // physical pages of this workgroup's keys
+  __shared__ __align__(16) int32_t pg[kMaxSplitKeys / kPage + 8];  // pages of this workgroup
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -125,7 +128,7 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
   const int qhead = kvh * G + g;
   const int last_task = min(tgrp * kWaves + kWaves - 1, sp.n_tasks - 1);
   const int last_q = min((last_task / G + 1) * kQB, sp.len);
-  // positions fit in int32 (the host checks the cache capacity)
+  // positions fit in int32 and element offsets within a layer in uint32 (host-checked)
   const int wg_keys = (int)sp.n_past + last_q;
   const int k_begin = split * sp.split_keys;
   const int k_end = min(k_begin + sp.split_keys, wg_keys);
@@ -155,76 +158,78 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
-  float m = -INFINITY, l = 0.f;
+  float m_ref = -INFINITY;   // reference max (log2 units) shared by l and o
+  float l = 0.f;             // this lane's share of the row sum (its key half)
 
-  const int64_t hstride = (int64_t)kPage * D;               // one (page, head) slab
-  const int64_t n_cols = (int64_t)a.n_phys_pages * kPage;   // transposed V row length
-  const uint16_t *kbase = a.kc + (int64_t)kvh * hstride;
-  const int64_t pstride = (int64_t)a.n_kv_heads * hstride;   // one physical page, all heads
+  const uint32_t pstride = (uint32_t)a.n_kv_heads * kPage * D;   // one physical page, all heads
+  const uint16_t *kbase = a.kc + (int64_t)kvh * kPage * D;
+  const uint16_t *vbase = a.vc + (int64_t)kvh * kPage * D;
+  const uint32_t n_cols = (uint32_t)a.n_phys_pages * kPage;        // transposed V row length
+  const uint16_t *vtbase = a.vc + (int64_t)kvh * D * n_cols;
 
-  // ---- global -> register staging of one tile
+  // ---- per-thread staging assignment (invariant over tiles)
   constexpr int K_ITEMS = KT * KCH / 256;                   // 16-byte K chunks per thread
   constexpr int V_ITEMS_RM = (KT / 4) * (D / 8);            // (4-token, 8-dim) groups
   constexpr int V_PER_T_RM = (V_ITEMS_RM + 255) / 256;
   constexpr int V_ITEMS_T = D * (KT / 8);                   // (dim, 8-token) groups
   constexpr int V_PER_T_T = V_ITEMS_T / 256;
   static_assert(K_ITEMS >= 1 && KT * KCH % 256 == 0, "tile too small");
-  uint4 kreg[K_ITEMS];
-  uint4 vreg[VT ? V_PER_T_T : 4 * V_PER_T_RM];
+  static_assert(V_PER_T_RM == 1 || VT, "one V group per thread");
+  u32x4 kreg[K_ITEMS];
+  u32x4 vreg[VT ? V_PER_T_T : 4];
+
+  // K: thread owns chunk kc of keys kkey[i]
+  const int kc = tid % KCH;
+  // V row-major: 4 tokens (4 vg4 .. 4 vg4 + 3) x 8 dims (8 vdc ..)
+  const int vg4 = tid / (D / 8), vdc = tid % (D / 8);
+  constexpr bool kAllOwnV = VT || V_ITEMS_RM >= 256;
+  const bool v_owner = kAllOwnV || tid < V_ITEMS_RM;
 
   __syncthreads();   // pg[] visible
 
-  auto page_of = [&](int t) -> int64_t { return pg[(t >> kPageShift) - pg0]; };
-
-  auto load_tile = [&](int kt) {
+  // Tokens past the split end are clamped to the last valid key k_end - 1: real cache data, so
+  // their K/V are finite; their scores are masked and their weights are exactly 0.  Global
+  // addresses are a uniform base plus a 32-bit unsigned byte offset.
+  const char *kbytes = reinterpret_cast<const char *>(kbase);
+  const char *vbytes = reinterpret_cast<const char *>(VT ? vtbase : vbase);
+  auto load_tile = [&](int it) {
+    const int kt = k_begin + it * KT;
+    const int tl = k_end - 1;
 #pragma unroll
     for (int i = 0; i < K_ITEMS; ++i) {
-      const int u = tid + 256 * i;
-      const int key = u / KCH, c = u % KCH;
-      const int t = kt + key;
-      if (t < k_end) {
-        kreg[i] = *reinterpret_cast<const uint4 *>(kbase + page_of(t) * pstride +
-                                                   (t & (kPage - 1)) * D + c * 8);
-      } else {
-        kreg[i] = make_uint4(0, 0, 0, 0);
-      }
+      const int key = (tid + 256 * i) / KCH;
+      const uint32_t t = (uint32_t)min(kt + key, tl);
+      const uint32_t page = (uint32_t)pg[(t >> kPageShift) - pg0];
+      const uint32_t off = (__umul24(page, pstride) + (t & (kPage - 1)) * D + kc * 8) * 2u;
+      kreg[i] = *reinterpret_cast<const u32x4 *>(kbytes + off);
     }
     if constexpr (!VT) {
-      const uint16_t *vbase = a.vc + (int64_t)kvh * hstride;
-#pragma unroll
-      for (int i = 0; i < V_PER_T_RM; ++i) {
-        const int u = tid + 256 * i;
+      if (kAllOwnV || v_owner) {
+        const uint32_t t0 = (uint32_t)min(kt + 4 * vg4, tl);
+        const uint32_t page = (uint32_t)pg[(t0 >> kPageShift) - pg0];
+        const uint32_t base = __umul24(page, pstride) + vdc * 8;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          uint4 val = make_uint4(0, 0, 0, 0);
-          if (u < V_ITEMS_RM) {
-            const int tg4 = u / (D / 8), dc = u % (D / 8);
-            const int t = kt + 4 * tg4 + e;
-            if (t < k_end)
-              val = *reinterpret_cast<const uint4 *>(vbase + page_of(t) * pstride +
-                                                     (t & (kPage - 1)) * D + dc * 8);
-          }
-          vreg[4 * i + e] = val;
+          const uint32_t t = (uint32_t)min(kt + 4 * vg4 + e, tl);
+          vreg[e] = *reinterpret_cast<const u32x4 *>(vbytes + (base + (t & (kPage - 1)) * D) * 2u);
         }
       }
     } else {
-      const uint16_t *vrow0 = a.vc + (int64_t)kvh * D * n_cols;
 #pragma unroll
       for (int i = 0; i < V_PER_T_T; ++i) {
         const int u = tid + 256 * i;
         const int d = u / (KT / 8), grp = u % (KT / 8);
-        const int t0 = kt + 8 * grp;
-        uint4 val = make_uint4(0, 0, 0, 0);
-        if (t0 < k_end) {
-          const uint16_t *src = vrow0 + (int64_t)d * n_cols + page_of(t0) * kPage + (t0 & (kPage - 1));
-          if (t0 + 8 <= k_end) {
-            val = *reinterpret_cast<const uint4 *>(src);
-          } else {
-            uint32_t w[4] = {0, 0, 0, 0};
-            for (int e = 0; e < 8; ++e)
-              if (t0 + e < k_end) w[e >> 1] |= (uint32_t)src[e] << (16 * (e & 1));
-            val = make_uint4(w[0], w[1], w[2], w[3]);
-          }
+        const int t0 = min(kt + 8 * grp, tl & ~7);   // 8-token group holding key t0
+        const uint32_t page = (uint32_t)pg[(t0 >> kPageShift) - pg0];
+        u32x4 val = *reinterpret_cast<const u32x4 *>(
+            vbytes + ((uint32_t)d * n_cols + page * kPage + (uint32_t)(t0 & (kPage - 1))) * 2u);
+        if (kt + 8 * grp + 8 > k_end) {
+          // group crosses or lies past the split end: keep keys <= tl, zero the rest (slots
+          // past the end of the written cache may hold anything)
+          const int nvalid = max(0, min(8, k_end - (kt + 8 * grp)));
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (e >= nvalid) val[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
         }
         vreg[i] = val;
       }
@@ -236,37 +241,23 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
     uint16_t *vs = Vs[buf];
 #pragma unroll
     for (int i = 0; i < K_ITEMS; ++i) {
-      const int u = tid + 256 * i;
-      const int key = u / KCH, c = u % KCH;
-      *reinterpret_cast<uint4 *>(ks + key * D + ((c ^ (key & KSW)) * 8)) = kreg[i];
+      const int key = (tid + 256 * i) / KCH;
+      *reinterpret_cast<u32x4 *>(ks + key * D + ((kc ^ (key & KSW)) * 8)) = kreg[i];
     }
     if constexpr (!VT) {
+      if (kAllOwnV || v_owner) {
+        const int pos = (4 * vg4 & ~15) | vt_pos(4 * vg4 & 15);   // 4-aligned
+        const int cc = pos >> 3, half = (pos >> 2) & 1;
 #pragma unroll
-      for (int i = 0; i < V_PER_T_RM; ++i) {
-        const int u = tid + 256 * i;
-        if (u < V_ITEMS_RM) {
-          const int tg4 = u / (D / 8), dc = u % (D / 8);
-          const int pos = (4 * tg4 & ~15) | vt_pos(4 * tg4 & 15);   // 4-aligned
-          const int cc = pos >> 3, half = (pos >> 2) & 1;
-          const uint32_t *w0 = reinterpret_cast<const uint32_t *>(&vreg[4 * i + 0]);
-          const uint32_t *w1 = reinterpret_cast<const uint32_t *>(&vreg[4 * i + 1]);
-          const uint32_t *w2 = reinterpret_cast<const uint32_t *>(&vreg[4 * i + 2]);
-          const uint32_t *w3 = reinterpret_cast<const uint32_t *>(&vreg[4 * i + 3]);
-#pragma unroll
-          for (int dd = 0; dd < 8; ++dd) {
-            const int wi = dd >> 1;
-            uint32_t lo, hi;
-            if (dd & 1) {
-              lo = (w0[wi] >> 16) | (w1[wi] & 0xFFFF0000u);
-              hi = (w2[wi] >> 16) | (w3[wi] & 0xFFFF0000u);
-            } else {
-              lo = (w0[wi] & 0xFFFFu) | (w1[wi] << 16);
-              hi = (w2[wi] & 0xFFFFu) | (w3[wi] << 16);
-            }
-            const int d = 8 * dc + dd;
-            *reinterpret_cast<uint2 *>(vs + d * KT + ((cc ^ vt_swz<VSW>(d)) * 8) + half * 4) =
-                make_uint2(lo, hi);
-          }
+        for (int dd = 0; dd < 8; ++dd) {
+          const int wi = dd >> 1;
+          // gather feature dd of the 4 tokens: low or high halves of word wi
+          const uint32_t sel = (dd & 1) ? 0x07060302u : 0x05040100u;
+          const uint32_t lo = __builtin_amdgcn_perm(vreg[1][wi], vreg[0][wi], sel);
+          const uint32_t hi = __builtin_amdgcn_perm(vreg[3][wi], vreg[2][wi], sel);
+          const int d = 8 * vdc + dd;
+          *reinterpret_cast<u32x2 *>(vs + d * KT + ((cc ^ vt_swz<VSW>(d)) * 8) + half * 4) =
+              u32x2{lo, hi};
         }
       }
     } else {
@@ -279,18 +270,21 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
           const int k4 = 8 * grp + 4 * hf;
           const int pos = (k4 & ~15) | vt_pos(k4 & 15);
           const int cc = pos >> 3, half = (pos >> 2) & 1;
-          const uint2 piece = hf ? make_uint2(vreg[i].z, vreg[i].w) : make_uint2(vreg[i].x, vreg[i].y);
-          *reinterpret_cast<uint2 *>(vs + d * KT + ((cc ^ vt_swz<VSW>(d)) * 8) + half * 4) = piece;
+          const u32x2 piece = hf ? u32x2{vreg[i][2], vreg[i][3]} : u32x2{vreg[i][0], vreg[i][1]};
+          *reinterpret_cast<u32x2 *>(vs + d * KT + ((cc ^ vt_swz<VSW>(d)) * 8) + half * 4) = piece;
         }
       }
     }
   };
 
+  const float c_scale = CAP ? 1.0f : a.scale_log2;   // raw score -> log2 units
+  const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+
   // ---- pipeline: tile t is in LDS buffer t & 1 while tile t + 1 waits in registers
   if (n_tiles > 0) {
-    load_tile(k_begin);
+    load_tile(0);
     store_tile(0);
-    if (n_tiles > 1) load_tile(k_begin + KT);
+    if (n_tiles > 1) load_tile(1);
   }
   __syncthreads();
   for (int it = 0; it < n_tiles; ++it) {
@@ -312,52 +306,54 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
           sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[s], sacc[kb], 0, 0, 0);
         }
       }
-
-      // ---- scores in log2 units, masking, online softmax
-      const bool need_mask = (kt + KT > k_end) || (kt + KT - 1 > qpos0);
-      const int my_pos = qpos0 + j;
+      if constexpr (CAP) {
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) sacc[kb][v] = a.cap_out * tanh_fast(sacc[kb][v] * a.cap_in);
+      }
+      // ---- causal / tail mask on tiles that cross this wave's diagonal or the split end
+      if ((kt + KT > k_end) || (kt + KT - 1 > qpos0)) {
+        const int lim = min(qpos0 + j, k_end - 1) - kt - 4 * hh;   // last visible key - base
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            if (32 * kb + 8 * (v >> 2) + (v & 3) > lim) sacc[kb][v] = -INFINITY;
+      }
+      // ---- online softmax (log2 units), lazily rescaled
       float mt = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          float x;
-          if constexpr (CAP) x = a.cap_out * tanh_fast(sacc[kb][v] * a.cap_in);
-          else x = sacc[kb][v] * a.scale_log2;
-          if (need_mask) {
-            const int key = kt + 32 * kb + 8 * (v >> 2) + 4 * hh + (v & 3);
-            if (key >= k_end || key > my_pos) x = -INFINITY;
-          }
-          sacc[kb][v] = x;
-          mt = fmaxf(mt, x);
-        }
-      mt = fmaxf(mt, __shfl_xor(mt, 32));
-      const float m_new = fmaxf(m, mt);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = fast_exp2(m - m_use);
-      float psum = 0.f;
+        for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sacc[kb][v]);
+      mt = fmaxf(mt, __shfl_xor(mt, 32)) * c_scale;
+      if (__builtin_amdgcn_ballot_w64(mt > m_ref + kSlack) != 0) {
+        const float m_new = fmaxf(m_ref, mt);
+        const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(m_ref - m_new);
+        l *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+        m_ref = m_new;
+      }
+      const float nm = (m_ref == -INFINITY) ? 0.f : -m_ref;
       bf16x8 pb[NKB][2];
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {
-          float p[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            p[e] = fast_exp2(sacc[kb][8 * hf + e] - m_use);
-            psum += p[e];
-          }
           uint32_t w[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(p[2 * e], p[2 * e + 1]);
+          for (int e = 0; e < 4; ++e) {
+            const float p0 = fast_exp2(fmaf(sacc[kb][8 * hf + 2 * e], c_scale, nm));
+            const float p1 = fast_exp2(fmaf(sacc[kb][8 * hf + 2 * e + 1], c_scale, nm));
+            w[e] = pack_bf16x2(p0, p1);
+            l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), ones, l, false);
+          }
           pb[kb][hf] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
         }
-      l = l * alpha + psum;
-      m = m_new;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
 
       // ---- O^T += V^T . P^T
 #pragma unroll
@@ -375,7 +371,7 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
         }
     }
     if (it + 1 < n_tiles) store_tile((it + 1) & 1);
-    if (it + 2 < n_tiles) load_tile(kt + 2 * KT);
+    if (it + 2 < n_tiles) load_tile(it + 2);
     __syncthreads();
   }
 
@@ -406,7 +402,7 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
         *reinterpret_cast<float4 *>(op + d0) =
             make_float4(o[db][4 * gq + 0], o[db][4 * gq + 1], o[db][4 * gq + 2], o[db][4 * gq + 3]);
       }
-    if (hh == 0) *reinterpret_cast<float2 *>(a.ws + sp.ml_off + prow * 2) = make_float2(m, l_tot);
+    if (hh == 0) *reinterpret_cast<float2 *>(a.ws + sp.ml_off + prow * 2) = make_float2(m_ref, l_tot);
   }
 }
 

@@ -59,7 +59,9 @@ nexus_status check_cache(const nexus_kv_cache *c) {
   if (!valid_layout(c->v_layout) || !valid_style(c->rope_style)) return NEXUS_EINVAL;
   if (!head_dim_ok(c->head_dim, es)) return NEXUS_ESHAPE;
   if (c->n_layers > 65535) return NEXUS_ESHAPE;
-  if ((int64_t)c->n_phys_pages * kPageSize * c->n_kv_heads >= kMaxElems32) return NEXUS_ESHAPE;
+  // kernels address one layer of K or V with 32-bit element offsets
+  if ((int64_t)c->n_phys_pages * kPageSize * c->n_kv_heads * c->head_dim >= kMaxElems32)
+    return NEXUS_ESHAPE;
   if (!(c->rope_base > 1.0) || !isfinite(c->rope_base)) return NEXUS_EROPE;
   return NEXUS_OK;
 }
