@@ -195,6 +195,9 @@ def main():
     ap.add_argument("--config", type=int, default=3, choices=[2, 3, 4, 5])
     ap.add_argument("--cpu-kv-sample", type=int, default=4,
                     help="KV heads of layer 0 the oracle baseline computes (0 skips it)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only time a plain device copy of MIB MiB (HBM reference and the "
+                         "scale of the FETCH_SIZE / WRITE_SIZE counters), then exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on one GPU only (no multi-GPU path); use --gpus 1",
@@ -202,6 +205,24 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").random_(0, 255)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = 20
+        a.record()
+        for _ in range(reps):
+            dst.copy_(src)
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / reps
+        print(json.dumps({"copy_mib": args.copy_calibration, "ms_per_copy": ms,
+                          "GBps_read_plus_write": 2 * n / (ms * 1e-3) / 1e9}), flush=True)
+        return
     from paper_2608_20397_amd import nexus as N
     N.lib()   # fail loudly if the library is not built
     torch.cuda.set_device(0)

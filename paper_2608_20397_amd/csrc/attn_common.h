@@ -1,0 +1,68 @@
+// Shared definitions of the bf16 suffix-attention kernels (internal, not part of the C ABI).
+#pragma once
+
+#include "device_common.h"
+
+namespace nexus {
+
+constexpr int kMaxSeqs = 32;
+constexpr int kWaves = 4;
+constexpr int kQB = 32;   // queries per wave task
+constexpr int kMaxSplitKeys = 16384;   // keys one workgroup covers at most
+
+struct SeqPlan {
+  int32_t q_start;     // first row of q / out
+  int32_t len;         // queries
+  int64_t n_past;      // position of the first query
+  int32_t row_begin;   // prefix sum of len over sequences (combine indexing)
+  int32_t first_unit;  // first (task group, split) unit of this sequence
+  int32_t n_tasks;     // group * ceil(len / 32)
+  int32_t n_splits;
+  int32_t split_keys;  // keys per split, a multiple of the key tile
+  int32_t pad_;
+  int64_t ws_off;      // float offset of the partial O of this sequence in the workspace
+  int64_t ml_off;      // float offset of its (m, l) pairs
+};
+
+struct AttnPlan {
+  SeqPlan seq[kMaxSeqs];
+  int32_t n_seqs;
+  int32_t units_per_head;
+  int32_t total_rows;
+  int32_t any_split;
+  size_t ws_bytes;
+};
+
+struct AttnArgs {
+  const uint16_t *q;
+  uint16_t *out;
+  const uint16_t *kc;   // layer base of the K cache
+  const uint16_t *vc;   // layer base of the V cache
+  const int32_t *map;
+  float *ws;
+  int32_t n_q_heads, n_kv_heads, group, n_phys_pages;
+  float scale_log2;     // scale * log2(e)
+  float cap_in;         // scale / softcap
+  float cap_out;        // softcap * log2(e)
+};
+
+__device__ __forceinline__ float tanh_fast(float x) {
+  // tanh x = 1 - 2 / (e^{2x} + 1); exp2 overflow to +inf gives 1, underflow to 0 gives -1.
+  const float e = fast_exp2(x * 2.8853900817779268f);  // 2 / ln 2
+  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(e + 1.0f);
+}
+
+// key index within a 16-key group -> its position in the V^T tile (swap bits 2 and 3)
+__device__ __forceinline__ int vt_pos(int k) {
+  return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1);
+}
+
+// V^T tile row swizzle: 16-byte chunk c of feature row d lives at chunk c ^ vt_swz(d).  Distinct
+// for 8 consecutive rows (conflict-free operand reads) and for rows 8 apart (tile writes).
+template <int VSW>
+__device__ __forceinline__ int vt_swz(int d) {
+  return (d ^ (d >> 3)) & VSW;
+}
+
+
+}  // namespace nexus

@@ -111,61 +111,72 @@ __global__ __launch_bounds__(256) void rephase_kernel(
     sd[e] = cs_tab[1][N * c + e];
   }
 
-  for (uint32_t r = gtid >> tpr_shift; r < n_rows; r += row_step) {
-    T *row;
-    if (map == nullptr) {
-      row = k + (uint64_t)r * head_dim;
-    } else {
-      const uint32_t l = fdiv(r, div_layer_rows);
-      const uint32_t rem = r - l * n_tokens * n_heads;
-      const uint32_t j = fdiv(rem, div_heads);
-      const uint32_t h = rem - j * n_heads;
-      const int64_t t = offset + j;
-      const uint64_t page = (uint32_t)map[t >> kPageShift];
-      row = k + ((((uint64_t)l * n_phys_pages + page) * n_heads + h) * kPage +
-                 (uint64_t)(t & (kPage - 1))) * head_dim;
-    }
-    uint4 *pa, *pb;
-    if constexpr (INTERLEAVED) {
-      pa = reinterpret_cast<uint4 *>(row + 2 * N * c);
-      pb = pa + 1;
-    } else {
-      pa = reinterpret_cast<uint4 *>(row + N * c);
-      pb = reinterpret_cast<uint4 *>(row + head_dim / 2 + N * c);
-    }
-    const uint4 va = *pa, vb = *pb;
-    float x[2 * N], a[N], b[N];
-    Pack<T>::unpack(va, x);
-    Pack<T>::unpack(vb, x + N);
-    if constexpr (INTERLEAVED) {
+  // rows in batches of kBatch: all loads of a batch are in flight before any rotation
+  constexpr int kBatch = 4;
+  auto row_ptr = [&](uint32_t r) -> T * {
+    if (map == nullptr) return k + (uint64_t)r * head_dim;
+    const uint32_t l = fdiv(r, div_layer_rows);
+    const uint32_t rem = r - l * n_tokens * n_heads;
+    const uint32_t j = fdiv(rem, div_heads);
+    const uint32_t h = rem - j * n_heads;
+    const int64_t t = offset + j;
+    const uint64_t page = (uint32_t)map[t >> kPageShift];
+    return k + ((((uint64_t)l * n_phys_pages + page) * n_heads + h) * kPage +
+                (uint64_t)(t & (kPage - 1))) * head_dim;
+  };
+  for (uint32_t r0 = gtid >> tpr_shift; r0 < n_rows; r0 += kBatch * row_step) {
+    uint4 *pa[kBatch], *pb[kBatch];
+    uint4 va[kBatch], vb[kBatch];
 #pragma unroll
-      for (int e = 0; e < N; ++e) {
-        a[e] = x[2 * e];
-        b[e] = x[2 * e + 1];
+    for (int u = 0; u < kBatch; ++u) {
+      const uint32_t r = r0 + u * row_step;
+      T *row = row_ptr(r < n_rows ? r : r0);
+      if constexpr (INTERLEAVED) {
+        pa[u] = reinterpret_cast<uint4 *>(row + 2 * N * c);
+        pb[u] = pa[u] + 1;
+      } else {
+        pa[u] = reinterpret_cast<uint4 *>(row + N * c);
+        pb[u] = reinterpret_cast<uint4 *>(row + head_dim / 2 + N * c);
       }
-    } else {
-#pragma unroll
-      for (int e = 0; e < N; ++e) {
-        a[e] = x[e];
-        b[e] = x[N + e];
-      }
+      va[u] = *pa[u];
+      vb[u] = *pb[u];
     }
-    rotate<Pack<T>, N>(a, b, cd, sd);
-    if constexpr (INTERLEAVED) {
 #pragma unroll
-      for (int e = 0; e < N; ++e) {
-        x[2 * e] = a[e];
-        x[2 * e + 1] = b[e];
-      }
-    } else {
+    for (int u = 0; u < kBatch; ++u) {
+      if (r0 + u * row_step >= n_rows) continue;
+      float x[2 * N], a[N], b[N];
+      Pack<T>::unpack(va[u], x);
+      Pack<T>::unpack(vb[u], x + N);
+      if constexpr (INTERLEAVED) {
 #pragma unroll
-      for (int e = 0; e < N; ++e) {
-        x[e] = a[e];
-        x[N + e] = b[e];
+        for (int e = 0; e < N; ++e) {
+          a[e] = x[2 * e];
+          b[e] = x[2 * e + 1];
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+          a[e] = x[e];
+          b[e] = x[N + e];
+        }
       }
+      rotate<Pack<T>, N>(a, b, cd, sd);
+      if constexpr (INTERLEAVED) {
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+          x[2 * e] = a[e];
+          x[2 * e + 1] = b[e];
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+          x[e] = a[e];
+          x[N + e] = b[e];
+        }
+      }
+      *pa[u] = Pack<T>::pack(x);
+      *pb[u] = Pack<T>::pack(x + N);
     }
-    *pa = Pack<T>::pack(x);
-    *pb = Pack<T>::pack(x + N);
   }
 }
 
