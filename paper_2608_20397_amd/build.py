@@ -30,9 +30,18 @@ FLAGS = [
 ]
 
 
+# Per-file code generation options.  The head_dim-128 attention kernel runs one wave per SIMD
+# with about 350 live registers; with MFMA accumulators in AGPRs (the backend's choice at that
+# budget) the register allocator copies O between the VGPR and AGPR files every key tile, so its
+# MFMAs are built in the VGPR-accumulator form.
+EXTRA = {
+    "attn_bf16_dma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(os.path.basename(src), []), "-x", "hip", "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

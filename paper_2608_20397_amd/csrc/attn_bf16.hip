@@ -26,6 +26,8 @@
 
 #include <stdlib.h>
 
+#include <algorithm>
+
 namespace nexus {
 
 template <int D, int KT, bool VT, bool CAP>
@@ -388,37 +390,61 @@ namespace {
 
 int key_tile_for(int head_dim) { return head_dim >= 256 ? 32 : 64; }
 
-int target_workgroups() {
-  static int t = [] {
-    const char *e = getenv("NEXUS_ATTN_TARGET_WGS");
-    const int v = e ? atoi(e) : 0;
-    return v > 0 ? v : 1024;
-  }();
-  return t;
+// Geometry of the kernel that serves a launch: queries per wave task, key tile, and how many
+// of its workgroups are resident per CU.
+struct KernelShape {
+  int qpw, key_tile, wgs_per_cu;
+};
+
+KernelShape kernel_shape(const AttnLaunch &p) {
+  if (p.head_dim == 128 && !p.v_transposed) return {kQPW_D128, 64, 1};
+  return {kQB, key_tile_for(p.head_dim), p.head_dim >= 256 ? 1 : 2};
 }
+
+constexpr int kCUs = 256;
 
 // Deterministic plan of an attention launch: task groups, key splits and workspace offsets.
 // The same arguments always give the same plan (the workspace query relies on it).
+// The split length is chosen to minimise the critical path, modelled as (rounds of resident
+// workgroups) x (keys per workgroup), with a small charge per extra split for the partials.
 bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   if (p.n_seqs < 1 || p.n_seqs > kMaxSeqs) return false;
   const int G = p.n_q_heads / p.n_kv_heads;
-  const int KT = key_tile_for(p.head_dim);
+  const KernelShape ks = kernel_shape(p);
+  const int KT = ks.key_tile;
+  const int64_t slots = (int64_t)kCUs * ks.wgs_per_cu;
   plan = AttnPlan{};
   plan.n_seqs = p.n_seqs;
-  double key_work = 0;
-  int64_t groups = 0;
-  for (int b = 0; b < p.n_seqs; ++b) {
-    const AttnSeq &s = p.seqs[b];
-    const int n_tasks = G * ((s.len + kQB - 1) / kQB);
-    const int n_tg = (n_tasks + kWaves - 1) / kWaves;
-    key_work += (double)n_tg * (double)(s.n_past + s.len);
-    groups += n_tg;
+  int64_t max_keys = 0;
+  for (int b = 0; b < p.n_seqs; ++b)
+    max_keys = std::max<int64_t>(max_keys, p.seqs[b].n_past + p.seqs[b].len);
+  auto n_tg_of = [&](const AttnSeq &s) {
+    const int n_tasks = G * ((s.len + ks.qpw - 1) / ks.qpw);
+    return (int64_t)((n_tasks + kWaves - 1) / kWaves);
+  };
+  int64_t best_sk = kMaxSplitKeys;
+  double best_cost = 1e300;
+  for (int ns = 1; ns <= 64; ++ns) {
+    int64_t sk = (max_keys + ns - 1) / ns;
+    sk = (sk + KT - 1) / KT * KT;
+    if (sk > kMaxSplitKeys) continue;
+    if (sk < 512 && ns > 1) break;
+    int64_t wgs = 0, max_splits = 1;
+    for (int b = 0; b < p.n_seqs; ++b) {
+      const int64_t keys = p.seqs[b].n_past + p.seqs[b].len;
+      const int64_t nsb = (keys + sk - 1) / sk;
+      max_splits = std::max(max_splits, nsb);
+      wgs += n_tg_of(p.seqs[b]) * nsb;
+    }
+    wgs *= p.n_kv_heads;
+    const double rounds = (double)((wgs + slots - 1) / slots);
+    const double cost = rounds * (double)std::min(sk, max_keys) * (1.0 + 0.03 * (max_splits - 1));
+    if (cost < best_cost - 1e-9) {
+      best_cost = cost;
+      best_sk = sk;
+    }
   }
-  const double per_wg = key_work * p.n_kv_heads / target_workgroups();
-  int64_t split_keys = (int64_t)per_wg;
-  if (split_keys < 512) split_keys = 512;
-  if (split_keys > kMaxSplitKeys) split_keys = kMaxSplitKeys;
-  split_keys = (split_keys + KT - 1) / KT * KT;
+  const int64_t split_keys = best_sk;
   int32_t unit = 0, rows = 0;
   int64_t ws_floats = 0;
   for (int b = 0; b < p.n_seqs; ++b) {
@@ -429,7 +455,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     sp.n_past = s.n_past;
     sp.row_begin = rows;
     sp.first_unit = unit;
-    sp.n_tasks = G * ((s.len + kQB - 1) / kQB);
+    sp.n_tasks = G * ((s.len + ks.qpw - 1) / ks.qpw);
     const int n_tg = (sp.n_tasks + kWaves - 1) / kWaves;
     const int64_t keys = s.n_past + s.len;
     int64_t ns = (keys + split_keys - 1) / split_keys;
@@ -453,7 +479,6 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   plan.units_per_head = unit;
   plan.total_rows = rows;
   plan.ws_bytes = (size_t)ws_floats * sizeof(float);
-  (void)groups;
   return true;
 }
 
