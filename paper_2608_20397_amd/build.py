@@ -30,13 +30,8 @@ FLAGS = [
 ]
 
 
-# Per-file code generation options.  The head_dim-128 attention kernel runs one wave per SIMD
-# with about 350 live registers; with MFMA accumulators in AGPRs (the backend's choice at that
-# budget) the register allocator copies O between the VGPR and AGPR files every key tile, so its
-# MFMAs are built in the VGPR-accumulator form.
-EXTRA = {
-    "attn_bf16_dma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
-}
+# Per-file code generation options (none at present).
+EXTRA: dict[str, list[str]] = {}
 
 
 def _compile(src: str) -> str:

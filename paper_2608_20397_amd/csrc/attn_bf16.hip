@@ -397,7 +397,7 @@ struct KernelShape {
 };
 
 KernelShape kernel_shape(const AttnLaunch &p) {
-  if (p.head_dim == 128 && !p.v_transposed) return {kQPW_D128, 64, 1};
+  if (p.head_dim == 128 && !p.v_transposed) return {kQB, 64, 2};
   return {kQB, key_tile_for(p.head_dim), p.head_dim >= 256 ? 1 : 2};
 }
 

@@ -7,8 +7,7 @@ namespace nexus {
 
 constexpr int kMaxSeqs = 32;
 constexpr int kWaves = 4;
-constexpr int kQB = 32;   // queries per wave task (generic kernel)
-constexpr int kQPW_D128 = 64;   // queries per wave task (head_dim-128 DMA kernel)
+constexpr int kQB = 32;   // queries per wave task
 constexpr int kMaxSplitKeys = 16384;   // keys one workgroup covers at most
 
 struct SeqPlan {
