@@ -18,6 +18,7 @@ the same workload on the host cores.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import subprocess
@@ -30,6 +31,38 @@ sys.path.insert(0, ROOT)
 MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 HBM_PEAK_GBPS = 8000.0           # MI355X HBM3E
 METRIC = "suffix-redecode attn TFLOP/s + re-phase/splice GB/s, % of MI355X roofline"
+
+# Measured HBM traffic of one attention call (rocprofv3 FETCH_SIZE / WRITE_SIZE, scaled by a
+# plain copy), valid only for the kernel sources it was taken on.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_attn_cfg3_qwen14b.txt")
+ATTN_SOURCES = ["attn_bf16_dma.hip", "attn_bf16.hip", "attn_common.h", "device_common.h",
+                "launch.h"]
+
+
+def attn_sources_sha() -> str:
+    h = hashlib.sha256()
+    for f in ATTN_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_20397_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(cfg: int):
+    """Bytes per attention call from the committed counter summary, or None when it was taken
+    on other kernel sources or another workload."""
+    try:
+        kv = {}
+        with open(TRAFFIC_FILE) as fh:
+            for line in fh:
+                if line.startswith("#") or ":" not in line:
+                    continue
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+        if kv.get("workload") != f"cfg{cfg}" or kv.get("kernel_sources_sha256") != attn_sources_sha():
+            return None
+        return int(kv["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def attn_flops(wl) -> float:
@@ -132,10 +165,12 @@ def run_step(S, events=None):
                 workspace=S["ws"]))
 
 
-def cpu_baseline(cfg: int, n_kv_sample: int):
-    """The fp64 oracle on a bounded sample: one layer's splice + re-anchor (all heads) and the
-    attention of ``n_kv_sample`` KV heads' query groups, scaled to the whole step."""
-    import numpy as np
+def cpu_baseline(cfg: int, n_kv_sample: int, n_layers: int):
+    """The fp64 oracle on a bounded sample: the first ``n_layers`` layers' splice + re-anchor
+    (all heads) and the attention of ``n_kv_sample`` KV heads' query groups, scaled to the
+    whole step."""
+    import dataclasses
+
     from threadpoolctl import threadpool_info
 
     import oracle as O
@@ -143,34 +178,35 @@ def cpu_baseline(cfg: int, n_kv_sample: int):
     from synth import gen as G
 
     wl = G.get_workload(cfg)
-    hc = G.host_case_wl(__import__("dataclasses").replace(wl, n_layers=1), cfg, layers=[0])
-    pm = hc.page_map
-    t0 = time.perf_counter()
-    ck, cv = G.empty_cache_bits(hc.wl, 1)
-    ck, cv = O.splice_paged(ck, cv, pm, hc.ctx_k, hc.ctx_v, 0, PAGE, wl.v_layout)
-    t_setup = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    for b, pos in enumerate(wl.splice_pos):
-        ck, cv = O.splice_paged(ck, cv, pm, hc.blk_k[b], hc.blk_v[b], pos, PAGE, wl.v_layout)
-        ck = O.rephase_paged_bits(ck, wl.dtype, pm, PAGE, pos, wl.block_len, wl.anchor, pos,
-                                  wl.rope_base)
-    if wl.n_user:
-        u0 = wl.splice_pos[0] + wl.block_len
-        ck, cv = O.splice_paged(ck, cv, pm, hc.user_k, hc.user_v, u0, PAGE, wl.v_layout)
-    t_splice = time.perf_counter() - t0
-    t0 = time.perf_counter()
+    n_layers = max(1, min(n_layers, wl.n_layers))
+    t_splice = t_attn = 0.0
     G_ = wl.group
-    n_keys = max(wl.attn_n_past) + wl.n_suffix
-    lk, lv = O.gather_logical(ck, cv, pm, n_keys, PAGE, wl.v_layout)
-    k = O.storage_to_f64(lk[0], wl.dtype)
-    v = O.storage_to_f64(lv[0], wl.dtype)
-    for b, n_past in enumerate(wl.attn_n_past):
-        qb = O.storage_to_f64(hc.q[0, b * wl.n_suffix:(b + 1) * wl.n_suffix], wl.dtype)
-        for g in range(n_kv_sample):
-            O.suffix_attention(qb[:, g * G_:(g + 1) * G_], k[:, g:g + 1], v[:, g:g + 1], n_past,
-                               softcap=wl.softcap)
-    t_attn = time.perf_counter() - t0
-    step_s = wl.n_layers * (t_splice + t_attn * wl.n_kv_heads / n_kv_sample)
+    for layer in range(n_layers):
+        hc = G.host_case_wl(dataclasses.replace(wl, n_layers=1), cfg, layers=[layer])
+        pm = hc.page_map
+        ck, cv = G.empty_cache_bits(hc.wl, 1)
+        ck, cv = O.splice_paged(ck, cv, pm, hc.ctx_k, hc.ctx_v, 0, PAGE, wl.v_layout)
+        t0 = time.perf_counter()
+        for b, pos in enumerate(wl.splice_pos):
+            ck, cv = O.splice_paged(ck, cv, pm, hc.blk_k[b], hc.blk_v[b], pos, PAGE, wl.v_layout)
+            ck = O.rephase_paged_bits(ck, wl.dtype, pm, PAGE, pos, wl.block_len, wl.anchor, pos,
+                                      wl.rope_base)
+        if wl.n_user:
+            u0 = wl.splice_pos[0] + wl.block_len
+            ck, cv = O.splice_paged(ck, cv, pm, hc.user_k, hc.user_v, u0, PAGE, wl.v_layout)
+        t_splice += time.perf_counter() - t0
+        t0 = time.perf_counter()
+        n_keys = max(wl.attn_n_past) + wl.n_suffix
+        lk, lv = O.gather_logical(ck, cv, pm, n_keys, PAGE, wl.v_layout)
+        k = O.storage_to_f64(lk[0], wl.dtype)
+        v = O.storage_to_f64(lv[0], wl.dtype)
+        for b, n_past in enumerate(wl.attn_n_past):
+            qb = O.storage_to_f64(hc.q[0, b * wl.n_suffix:(b + 1) * wl.n_suffix], wl.dtype)
+            for g in range(n_kv_sample):
+                O.suffix_attention(qb[:, g * G_:(g + 1) * G_], k[:, g:g + 1], v[:, g:g + 1],
+                                   n_past, softcap=wl.softcap)
+        t_attn += time.perf_counter() - t0
+    step_s = (wl.n_layers / n_layers) * (t_splice + t_attn * wl.n_kv_heads / n_kv_sample)
     flops = attn_flops(wl) * wl.n_layers
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {
@@ -178,9 +214,9 @@ def cpu_baseline(cfg: int, n_kv_sample: int):
         "unit": "TFLOP/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": (f"layer 0 only: splice + re-anchor of all {wl.n_kv_heads} KV heads "
+        "sample": (f"layers 0..{n_layers - 1}: splice + re-anchor of all {wl.n_kv_heads} KV heads "
                    f"({t_splice:.2f} s) and attention of {n_kv_sample} of {wl.n_kv_heads} KV-head "
-                   f"query groups ({t_attn:.2f} s), scaled x{wl.n_layers} layers and "
+                   f"query groups ({t_attn:.2f} s), scaled x{wl.n_layers / n_layers:g} layers and "
                    f"x{wl.n_kv_heads / n_kv_sample:g} heads to one step; fp64 numpy, BLAS threads "
                    f"for the matmuls, elementwise exp single-threaded"),
         "step_s_estimate": step_s,
@@ -193,8 +229,10 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3, choices=[2, 3, 4, 5])
-    ap.add_argument("--cpu-kv-sample", type=int, default=4,
-                    help="KV heads of layer 0 the oracle baseline computes (0 skips it)")
+    ap.add_argument("--cpu-kv-sample", type=int, default=8,
+                    help="KV heads per layer the oracle baseline computes (0 skips it)")
+    ap.add_argument("--cpu-layers", type=int, default=3,
+                    help="layers the oracle baseline computes")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only time a plain device copy of MIB MiB (HBM reference and the "
                          "scale of the FETCH_SIZE / WRITE_SIZE counters), then exit")
@@ -282,12 +320,14 @@ def main():
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": "nexus_suffix_attn (attn_bf16_kernel + split combine), per layer",
+            "kernel": ("one nexus_suffix_attn call per layer: attn_bf16_d128_dma_kernel + "
+                       "attn_combine_kernel (split-K combine)"),
             "achieved": attn_tflops,
             "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": attn_tflops / MFMA_BF16_PEAK_TFLOPS,
-            "traffic": None,
+            "traffic": measured_traffic(wl.cfg),
+            "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-scaled)",
             "algorithmic_flops_per_launch": fl_layer,
             "mean_launch_ms": mean["attn"],
         },
@@ -310,7 +350,8 @@ def main():
         res["git"] = None
     if args.cpu_kv_sample > 0:
         print("bench: timing the oracle baseline on the host", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(args.config, min(args.cpu_kv_sample, wl.n_kv_heads))
+        res["cpu_baseline"] = cpu_baseline(args.config, min(args.cpu_kv_sample, wl.n_kv_heads),
+                                           args.cpu_layers)
     print(json.dumps(res), flush=True)
 
 
