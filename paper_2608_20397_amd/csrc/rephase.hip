@@ -3,10 +3,12 @@
 // (the inverse of the drift of eq. (drift)).  In place; V is never touched.
 //
 // HBM-bound: each workgroup forms the D/2 angles once in fp64 (reduced modulo 2*pi in fp64) and
-// keeps their cosine and sine (fp64) in LDS; each thread owns a fixed group of feature pairs,
-// holds their cos/sin in registers and streams rows with 16-byte loads and stores.  The rotation
-// runs in fp64 and is rounded once to the storage type (nearest-even), so near-zero results do
-// not suffer fp32 cancellation.
+// keeps their cosine and sine in LDS as fp32 head + tail pairs (c = c_hi + c_lo to about 2^-48);
+// each thread owns a fixed group of feature pairs, holds their cos/sin in registers and streams
+// rows with 16-byte loads and stores.  The rotation x c - y s is evaluated in fp32 with the
+// product y s_hi split exactly by an FMA (Dekker's two-product) and the tail terms added
+// separately, so the fp32 result is within about 2^-23 relative of the exact rotation even
+// when the two products cancel; it is then rounded to the storage type (nearest-even).
 #include "device_common.h"
 #include "launch.h"
 
@@ -42,12 +44,6 @@ struct Pack<uint16_t> {  // 8 bf16
       x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
     }
   }
-  // fp64 -> bf16 with one rounding: round-to-odd into fp32 (24 >= 8 + 2 bits), then the
-  // nearest-even fp32 -> bf16 conversion.
-  __device__ static float to_odd(double x) {
-    const float f = __double2float_rz(x);
-    return ((double)f == x) ? f : __uint_as_float(__float_as_uint(f) | 1u);
-  }
   __device__ static uint4 pack(const float *x) {
     uint4 v;
     v.x = pack_bf16x2(x[0], x[1]);
@@ -61,7 +57,6 @@ struct Pack<uint16_t> {  // 8 bf16
 template <>
 struct Pack<uint32_t> {  // 4 f32
   static constexpr int N = 4;
-  __device__ static float to_odd(double x) { return (float)x; }  // f32 keys: one RNE rounding
   __device__ static void unpack(const uint4 &v, float *x) {
     x[0] = __uint_as_float(v.x);
     x[1] = __uint_as_float(v.y);
@@ -74,14 +69,25 @@ struct Pack<uint32_t> {  // 4 f32
   }
 };
 
-// Rotate pairs (a[e], b[e]) by (c[e], s[e]) in fp64.
-template <typename P, int N>
-__device__ __forceinline__ void rotate(float *a, float *b, const double *c, const double *s) {
+// u c - w s with c = ch + cl, s = sh + sl: w sh = p + e exactly (two-product by FMA), then
+// (u ch - p) rounded once by an FMA, plus the small terms (u cl - w sl) - e.
+__device__ __forceinline__ float rot_dot(float u, float w, float ch, float cl, float sh, float sl) {
+  const float p = w * sh;
+  const float e = fmaf(w, sh, -p);
+  const float r = fmaf(u, ch, -p);
+  const float t = fmaf(u, cl, -(w * sl));
+  return r + (t - e);
+}
+
+// Rotate pairs (a[e], b[e]) by the angle whose cos/sin head and tail are (ch, cl, sh, sl)[e].
+template <int N>
+__device__ __forceinline__ void rotate(float *a, float *b, const float *ch, const float *cl,
+                                       const float *sh, const float *sl) {
 #pragma unroll
   for (int e = 0; e < N; ++e) {
-    const double xa = a[e], xb = b[e];
-    a[e] = P::to_odd(xa * c[e] - xb * s[e]);
-    b[e] = P::to_odd(xa * s[e] + xb * c[e]);
+    const float xa = a[e], xb = b[e];
+    a[e] = rot_dot(xa, xb, ch[e], cl[e], sh[e], sl[e]);      // xa c - xb s
+    b[e] = rot_dot(xb, -xa, ch[e], cl[e], sh[e], sl[e]);     // xb c + xa s
   }
 }
 
@@ -95,20 +101,29 @@ __global__ __launch_bounds__(256) void rephase_kernel(
     uint32_t tpr_shift, FastDiv div_heads, FastDiv div_layer_rows, uint32_t n_heads,
     uint32_t n_tokens, uint32_t n_phys_pages, int32_t head_dim, int64_t delta, double base) {
   constexpr int N = Pack<T>::N;
-  __shared__ double cs_tab[2][kMaxPairs];
-  for (int i = threadIdx.x; i < head_dim / 2; i += blockDim.x)
-    pair_angle(delta, base, i, head_dim, cs_tab[0][i], cs_tab[1][i]);
+  __shared__ float cs_tab[4][kMaxPairs];   // cos head, cos tail, sin head, sin tail
+  for (int i = threadIdx.x; i < head_dim / 2; i += blockDim.x) {
+    double c, sn;
+    pair_angle(delta, base, i, head_dim, c, sn);
+    const float ch = (float)c, sh = (float)sn;
+    cs_tab[0][i] = ch;
+    cs_tab[1][i] = (float)(c - (double)ch);
+    cs_tab[2][i] = sh;
+    cs_tab[3][i] = (float)(sn - (double)sh);
+  }
   __syncthreads();
 
   const uint32_t tpr = 1u << tpr_shift;  // threads per row
   const uint32_t gtid = blockIdx.x * blockDim.x + threadIdx.x;
   const uint32_t c = gtid & (tpr - 1);
   const uint32_t row_step = (gridDim.x * blockDim.x) >> tpr_shift;
-  double cd[N], sd[N];
+  float ch[N], cl[N], sh[N], sl[N];
 #pragma unroll
   for (int e = 0; e < N; ++e) {
-    cd[e] = cs_tab[0][N * c + e];
-    sd[e] = cs_tab[1][N * c + e];
+    ch[e] = cs_tab[0][N * c + e];
+    cl[e] = cs_tab[1][N * c + e];
+    sh[e] = cs_tab[2][N * c + e];
+    sl[e] = cs_tab[3][N * c + e];
   }
 
   // rows in batches of kBatch: all loads of a batch are in flight before any rotation
@@ -160,7 +175,7 @@ __global__ __launch_bounds__(256) void rephase_kernel(
           b[e] = x[N + e];
         }
       }
-      rotate<Pack<T>, N>(a, b, cd, sd);
+      rotate<N>(a, b, ch, cl, sh, sl);
       if constexpr (INTERLEAVED) {
 #pragma unroll
         for (int e = 0; e < N; ++e) {
