@@ -223,6 +223,51 @@ def cpu_baseline(cfg: int, n_kv_sample: int, n_layers: int):
     }
 
 
+def time_next_rows(S, reps: int):
+    """The one-pass splice + re-anchor of the block(s) and the rope-append of the suffix tokens,
+    timed alone after the measured steps (they are not part of a step).  GB/s on algorithmic
+    bytes: read + write of the block's K and V (the separate calls move 4 |K| + 2 |K|), and read
+    + write of the appended tokens' K and V."""
+    import torch
+    from paper_2608_20397_amd import nexus as N
+    wl, cache = S["wl"], S["cache"]
+    esize = 2 if wl.dtype == "bf16" else 4
+    L, H, D = wl.n_layers, wl.n_kv_heads, wl.head_dim
+
+    def timeit(fn):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(max(reps, 3)):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        return sum(ts) / len(ts)
+
+    out = {}
+    blk_bytes = L * wl.block_len * H * D * esize
+    for b, pos in enumerate(wl.splice_pos[:1]):
+        blk = S["blocks"][b]
+        ms = timeit(lambda: N.splice_rephase_pages(cache, blk, pos, pos))
+        out["splice_rephase_fused"] = {
+            "mean_launch_ms": ms, "bytes_per_launch": 4 * blk_bytes,
+            "achieved_GBps": 4 * blk_bytes / (ms * 1e-3) / 1e9,
+            "frac": 4 * blk_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+    n_app = wl.n_suffix
+    k_new = S["q"].new_empty((L, n_app, H, D)).normal_()
+    v_new = torch.empty_like(k_new).normal_()
+    off = wl.n_tokens - n_app
+    ms = timeit(lambda: N.rope_append(cache, k_new, v_new, off, off))
+    nbytes = 4 * L * n_app * H * D * esize
+    out["rope_append"] = {
+        "tokens": n_app, "mean_launch_ms": ms, "bytes_per_launch": nbytes,
+        "achieved_GBps": nbytes / (ms * 1e-3) / 1e9, "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -343,6 +388,7 @@ def main():
             "frac": rs_gbps / HBM_PEAK_GBPS,
         },
     }
+    res["next_rows"] = time_next_rows(S, args.steps)
     try:
         res["git"] = subprocess.run(["git", "-C", ROOT, "rev-parse", "--short", "HEAD"],
                                     capture_output=True, text=True).stdout.strip() or None

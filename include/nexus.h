@@ -109,9 +109,10 @@ typedef struct nexus_page_table {
  * Re-anchor every key of a compiled block, in place (Sec. III-B, eq. drift).
  * Rotates each key pair i of every layer, token and head of block->k by
  * (dst_pos - src_pos) * theta_i; V is never touched.  The angle is formed and reduced modulo
- * 2*pi in fp64, its cosine and sine are taken once per pair in fp64 and rounded to fp32, the
- * rotation is computed in fp32 (bf16 keys) or fp64 (f32 keys) and rounded to nearest-even back
- * into the block.  dst_pos == src_pos enqueues nothing, leaving the keys bit-identical.
+ * 2*pi in fp64 and its cosine and sine taken in fp64 and held as fp32 head + tail pairs; the
+ * rotation is evaluated in fp32 with compensated products (within about 2^-23 of the exact
+ * rotation) and rounded to nearest-even back into the block.  dst_pos == src_pos enqueues
+ * nothing, leaving the keys bit-identical.
  * Checks: src_pos == block->base_pos and rope_base == block->rope_base (else NEXUS_EROPE);
  * positions >= 0 (NEXUS_ERANGE).  On success block->base_pos (a host field) becomes dst_pos.
  */
@@ -142,6 +143,34 @@ nexus_status nexus_rephase_k_paged(const nexus_kv_cache *cache, const nexus_page
  */
 nexus_status nexus_splice_pages(const nexus_kv_cache *cache, const nexus_page_table *pt,
                                 const nexus_block *block, int64_t offset, void *stream);
+
+/*
+ * Splice a block and re-anchor its keys in one pass (Sec. III-B with Sec. VI-A): the cache ends
+ * bit-identical to nexus_splice_pages(cache, pt, block, offset) followed by
+ * nexus_rephase_k_paged(cache, pt, offset, block->n_tokens, block->base_pos, dst_pos, ...),
+ * while the block's keys are read once and each cache element is written once.  The block is
+ * not modified (block->base_pos keeps its value).  Checks: those of nexus_splice_pages, plus
+ * dst_pos >= 0 (NEXUS_ERANGE) and head_dim <= 256 (NEXUS_ESHAPE).  dst_pos == block->base_pos
+ * is a plain splice.
+ */
+nexus_status nexus_splice_rephase_pages(const nexus_kv_cache *cache, const nexus_page_table *pt,
+                                        const nexus_block *block, int64_t offset,
+                                        int64_t dst_pos, void *stream);
+
+/*
+ * Append freshly computed tokens (the redecode writes of Sec. VI-A): k and v are
+ * [cache->n_layers][n_tokens][cache->n_kv_heads][cache->head_dim] device arrays of the cache
+ * dtype holding UN-rotated keys and values.  Key token j is rotated to absolute position
+ * pos0 + j (RoPE with the cache's base and pairing, Sec. III-B; same arithmetic as
+ * nexus_rephase_k) and written, with value token j, into logical slot offset + j of every layer
+ * and KV head.  No other cache element is written; k and v are not modified.
+ * Checks: k, v non-NULL and n_tokens > 0 (NEXUS_EINVAL); offset >= 0, pos0 >= 0 and
+ * offset + n_tokens within the mapped logical pages (NEXUS_ERANGE); head_dim <= 256
+ * (NEXUS_ESHAPE).
+ */
+nexus_status nexus_rope_append(const nexus_kv_cache *cache, const nexus_page_table *pt,
+                               const void *k, const void *v, int32_t n_tokens, int64_t offset,
+                               int64_t pos0, void *stream);
 
 /*
  * Causal grouped-query attention of the re-decoded suffix (Sec. III-A; the suffix of Sec. VI-A).

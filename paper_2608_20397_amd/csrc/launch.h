@@ -15,8 +15,24 @@ struct SpliceLaunch {
   int32_t n_layers, n_tokens, n_heads, head_dim, n_phys_pages;
   int32_t dtype_bytes;             // 2 (bf16) or 4 (f32)
   bool v_transposed;
+  bool v_only = false;             // skip the K rows (they are written elsewhere)
 };
 hipError_t launch_splice(const SpliceLaunch &p, hipStream_t stream);
+
+// Keys rotated on the way into the pages: splice + re-anchor (angle0 = dst - src, the same
+// rotation for every token) or rope-append (per_token: token j rotated to position angle0 + j).
+struct RopeSpliceLaunch {
+  const void *src_k, *src_v;       // [L][T][H][D]
+  void *cache_k, *cache_v;         // as SpliceLaunch
+  const int32_t *map;
+  int64_t offset;
+  int32_t n_layers, n_tokens, n_heads, head_dim, n_phys_pages;
+  int32_t dtype_bytes;
+  bool v_transposed, interleaved, per_token;
+  int64_t angle0;
+  double rope_base;
+};
+hipError_t launch_rope_splice(const RopeSpliceLaunch &p, hipStream_t stream);
 
 struct RephaseLaunch {
   void *k;                 // block [L][T][H][D] (map == nullptr) or paged cache [L][NPP][H][16][D]

@@ -237,8 +237,11 @@ nexus_status nexus_rephase_k_paged(const nexus_kv_cache *cache, const nexus_page
   return from_hip(launch_rephase(L, as_stream(stream)));
 }
 
-nexus_status nexus_splice_pages(const nexus_kv_cache *cache, const nexus_page_table *pt,
-                                const nexus_block *block, int64_t offset, void *stream) {
+namespace {
+
+// The fail-closed checks of a splice (the block header against the cache, Sec. VI-A).
+nexus_status check_splice(const nexus_kv_cache *cache, const nexus_page_table *pt,
+                          const nexus_block *block, int64_t offset) {
   nexus_status st = check_cache(cache);
   if (st) return st;
   st = check_block(block);
@@ -256,6 +259,37 @@ nexus_status nexus_splice_pages(const nexus_kv_cache *cache, const nexus_page_ta
   const int es = dtype_bytes(cache->dtype);
   if (cache->v_layout == NEXUS_V_TRANSPOSED && (size_t)64 * (cache->head_dim + 16 / es) * es > 65536)
     return NEXUS_ESHAPE;
+  return NEXUS_OK;
+}
+
+RopeSpliceLaunch rope_splice_launch(const nexus_kv_cache *cache, const nexus_page_table *pt,
+                                    const void *k, const void *v, int32_t n_tokens,
+                                    int64_t offset) {
+  RopeSpliceLaunch L{};
+  L.src_k = k;
+  L.src_v = v;
+  L.cache_k = cache->k;
+  L.cache_v = cache->v;
+  L.map = pt->map;
+  L.offset = offset;
+  L.n_layers = cache->n_layers;
+  L.n_tokens = n_tokens;
+  L.n_heads = cache->n_kv_heads;
+  L.head_dim = cache->head_dim;
+  L.n_phys_pages = cache->n_phys_pages;
+  L.dtype_bytes = dtype_bytes(cache->dtype);
+  L.v_transposed = cache->v_layout == NEXUS_V_TRANSPOSED;
+  L.interleaved = cache->rope_style == NEXUS_ROPE_INTERLEAVED;
+  L.rope_base = cache->rope_base;
+  return L;
+}
+
+}  // namespace
+
+nexus_status nexus_splice_pages(const nexus_kv_cache *cache, const nexus_page_table *pt,
+                                const nexus_block *block, int64_t offset, void *stream) {
+  const nexus_status st = check_splice(cache, pt, block, offset);
+  if (st) return st;
   SpliceLaunch L{};
   L.block_k = block->k;
   L.block_v = block->v;
@@ -268,9 +302,46 @@ nexus_status nexus_splice_pages(const nexus_kv_cache *cache, const nexus_page_ta
   L.n_heads = cache->n_kv_heads;
   L.head_dim = cache->head_dim;
   L.n_phys_pages = cache->n_phys_pages;
-  L.dtype_bytes = es;
+  L.dtype_bytes = dtype_bytes(cache->dtype);
   L.v_transposed = cache->v_layout == NEXUS_V_TRANSPOSED;
   return from_hip(launch_splice(L, as_stream(stream)));
+}
+
+nexus_status nexus_splice_rephase_pages(const nexus_kv_cache *cache, const nexus_page_table *pt,
+                                        const nexus_block *block, int64_t offset,
+                                        int64_t dst_pos, void *stream) {
+  const nexus_status st = check_splice(cache, pt, block, offset);
+  if (st) return st;
+  if (dst_pos < 0) return NEXUS_ERANGE;
+  if (cache->head_dim > 256) return NEXUS_ESHAPE;
+  if (dst_pos == block->base_pos) return nexus_splice_pages(cache, pt, block, offset, stream);
+  RopeSpliceLaunch L = rope_splice_launch(cache, pt, block->k, block->v, block->n_tokens, offset);
+  L.per_token = false;
+  L.angle0 = dst_pos - block->base_pos;
+  return from_hip(launch_rope_splice(L, as_stream(stream)));
+}
+
+nexus_status nexus_rope_append(const nexus_kv_cache *cache, const nexus_page_table *pt,
+                               const void *k, const void *v, int32_t n_tokens, int64_t offset,
+                               int64_t pos0, void *stream) {
+  nexus_status st = check_cache(cache);
+  if (st) return st;
+  st = check_pt(pt, cache);
+  if (st) return st;
+  if (k == nullptr || v == nullptr || n_tokens <= 0) return NEXUS_EINVAL;
+  if (offset < 0 || pos0 < 0 || offset + n_tokens > (int64_t)pt->n_logical_pages * kPageSize)
+    return NEXUS_ERANGE;
+  if (cache->head_dim > 256) return NEXUS_ESHAPE;
+  if ((int64_t)n_tokens * cache->n_kv_heads * cache->head_dim >= kMaxElems32 ||
+      (int64_t)cache->n_layers * n_tokens * cache->n_kv_heads >= kMaxElems32)
+    return NEXUS_ESHAPE;
+  const int es = dtype_bytes(cache->dtype);
+  if (cache->v_layout == NEXUS_V_TRANSPOSED && (size_t)64 * (cache->head_dim + 16 / es) * es > 65536)
+    return NEXUS_ESHAPE;
+  RopeSpliceLaunch L = rope_splice_launch(cache, pt, k, v, n_tokens, offset);
+  L.per_token = true;
+  L.angle0 = pos0;
+  return from_hip(launch_rope_splice(L, as_stream(stream)));
 }
 
 size_t nexus_suffix_attn_workspace(int32_t n_s, int32_t n_q_heads, const nexus_kv_cache *cache,

@@ -9,89 +9,10 @@
 // product y s_hi split exactly by an FMA (Dekker's two-product) and the tail terms added
 // separately, so the fp32 result is within about 2^-23 relative of the exact rotation even
 // when the two products cancel; it is then rounded to the storage type (nearest-even).
-#include "device_common.h"
 #include "launch.h"
+#include "rope_math.h"
 
 namespace nexus {
-
-namespace {
-
-constexpr double kTwoPiHi = 6.283185307179586232;       // fp64(2*pi)
-constexpr double kTwoPiLo = 2.4492935982947064e-16;     // 2*pi - fp64(2*pi)
-constexpr int kMaxPairs = 512;                            // head_dim <= 1024
-
-__device__ __forceinline__ void pair_angle(int64_t delta, double base, int i, int head_dim,
-                                           double &c, double &s) {
-  const double theta = pow(base, -2.0 * (double)i / (double)head_dim);
-  const double ang = (double)delta * theta;
-  const double k = rint(ang / kTwoPiHi);
-  double r = fma(-k, kTwoPiHi, ang);
-  r = fma(-k, kTwoPiLo, r);
-  sincos(r, &s, &c);
-}
-
-template <typename T>
-struct Pack;  // 16 bytes of keys
-
-template <>
-struct Pack<uint16_t> {  // 8 bf16
-  static constexpr int N = 8;
-  __device__ static void unpack(const uint4 &v, float *x) {
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      x[2 * e] = __uint_as_float(w[e] << 16);
-      x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
-    }
-  }
-  __device__ static uint4 pack(const float *x) {
-    uint4 v;
-    v.x = pack_bf16x2(x[0], x[1]);
-    v.y = pack_bf16x2(x[2], x[3]);
-    v.z = pack_bf16x2(x[4], x[5]);
-    v.w = pack_bf16x2(x[6], x[7]);
-    return v;
-  }
-};
-
-template <>
-struct Pack<uint32_t> {  // 4 f32
-  static constexpr int N = 4;
-  __device__ static void unpack(const uint4 &v, float *x) {
-    x[0] = __uint_as_float(v.x);
-    x[1] = __uint_as_float(v.y);
-    x[2] = __uint_as_float(v.z);
-    x[3] = __uint_as_float(v.w);
-  }
-  __device__ static uint4 pack(const float *x) {
-    return make_uint4(__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]),
-                      __float_as_uint(x[3]));
-  }
-};
-
-// u c - w s with c = ch + cl, s = sh + sl: w sh = p + e exactly (two-product by FMA), then
-// (u ch - p) rounded once by an FMA, plus the small terms (u cl - w sl) - e.
-__device__ __forceinline__ float rot_dot(float u, float w, float ch, float cl, float sh, float sl) {
-  const float p = w * sh;
-  const float e = fmaf(w, sh, -p);
-  const float r = fmaf(u, ch, -p);
-  const float t = fmaf(u, cl, -(w * sl));
-  return r + (t - e);
-}
-
-// Rotate pairs (a[e], b[e]) by the angle whose cos/sin head and tail are (ch, cl, sh, sl)[e].
-template <int N>
-__device__ __forceinline__ void rotate(float *a, float *b, const float *ch, const float *cl,
-                                       const float *sh, const float *sl) {
-#pragma unroll
-  for (int e = 0; e < N; ++e) {
-    const float xa = a[e], xb = b[e];
-    a[e] = rot_dot(xa, xb, ch[e], cl[e], sh[e], sl[e]);      // xa c - xb s
-    b[e] = rot_dot(xb, -xa, ch[e], cl[e], sh[e], sl[e]);     // xb c + xa s
-  }
-}
-
-}  // namespace
 
 // NEOX: thread chunk c owns pairs [N c, N c + N): elements [N c, +N) and [D/2 + N c, +N).
 // INTERLEAVED: thread chunk c owns elements [2 N c, 2 N c + 2 N) = pairs [N c, N c + N).
@@ -102,15 +23,8 @@ __global__ __launch_bounds__(256) void rephase_kernel(
     uint32_t n_tokens, uint32_t n_phys_pages, int32_t head_dim, int64_t delta, double base) {
   constexpr int N = Pack<T>::N;
   __shared__ float cs_tab[4][kMaxPairs];   // cos head, cos tail, sin head, sin tail
-  for (int i = threadIdx.x; i < head_dim / 2; i += blockDim.x) {
-    double c, sn;
-    pair_angle(delta, base, i, head_dim, c, sn);
-    const float ch = (float)c, sh = (float)sn;
-    cs_tab[0][i] = ch;
-    cs_tab[1][i] = (float)(c - (double)ch);
-    cs_tab[2][i] = sh;
-    cs_tab[3][i] = (float)(sn - (double)sh);
-  }
+  for (int i = threadIdx.x; i < head_dim / 2; i += blockDim.x)
+    pair_cs(delta, base, i, head_dim, cs_tab[0][i], cs_tab[1][i], cs_tab[2][i], cs_tab[3][i]);
   __syncthreads();
 
   const uint32_t tpr = 1u << tpr_shift;  // threads per row
@@ -140,18 +54,18 @@ __global__ __launch_bounds__(256) void rephase_kernel(
                 (uint64_t)(t & (kPage - 1))) * head_dim;
   };
   for (uint32_t r0 = gtid >> tpr_shift; r0 < n_rows; r0 += kBatch * row_step) {
-    uint4 *pa[kBatch], *pb[kBatch];
-    uint4 va[kBatch], vb[kBatch];
+    u32x4 *pa[kBatch], *pb[kBatch];
+    u32x4 va[kBatch], vb[kBatch];
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const uint32_t r = r0 + u * row_step;
       T *row = row_ptr(r < n_rows ? r : r0);
       if constexpr (INTERLEAVED) {
-        pa[u] = reinterpret_cast<uint4 *>(row + 2 * N * c);
+        pa[u] = reinterpret_cast<u32x4 *>(row + 2 * N * c);
         pb[u] = pa[u] + 1;
       } else {
-        pa[u] = reinterpret_cast<uint4 *>(row + N * c);
-        pb[u] = reinterpret_cast<uint4 *>(row + head_dim / 2 + N * c);
+        pa[u] = reinterpret_cast<u32x4 *>(row + N * c);
+        pb[u] = reinterpret_cast<u32x4 *>(row + head_dim / 2 + N * c);
       }
       va[u] = *pa[u];
       vb[u] = *pb[u];

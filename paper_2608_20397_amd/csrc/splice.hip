@@ -121,7 +121,7 @@ hipError_t launch_splice(const SpliceLaunch &p, hipStream_t stream) {
   while ((1u << shift) < chunks_per_row) ++shift;
   const uint64_t items = (uint64_t)p.n_tokens * p.n_heads * chunks_per_row;
   const int n_kv = p.v_transposed ? 1 : 2;
-  {
+  if (!p.v_only) {
     const uint32_t threads = 256;
     uint64_t want = (items + threads * 4 - 1) / (threads * 4);
     const uint32_t blocks = (uint32_t)(want < 1 ? 1 : (want > 65535 ? 65535 : want));

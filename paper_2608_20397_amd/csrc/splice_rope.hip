@@ -1,0 +1,187 @@
+// Keys rotated on their way into the paged cache, in one pass over the source rows:
+//   * splice + re-anchor (Sec. III-B with Sec. VI-A): block key token j, compiled at anchor m0,
+//     is rotated by (dst - m0) * theta_i and written to logical slot offset + j; its value row
+//     is copied.  Same arithmetic as rephase_kernel, so the cache ends bit-identical to a
+//     splice followed by an in-place re-anchor, while the block's keys are read once and every
+//     cache element is written once;
+//   * rope-append (the redecode writes of Sec. VI-A): freshly computed, un-rotated key token j
+//     is rotated to its absolute position pos0 + j (RoPE, Sec. III-B) and written with its value
+//     row to logical slot offset + j.
+// A workgroup covers kTileTokens tokens of kLayersPerGroup layers, all heads.  It first forms,
+// in fp64, the cosine and sine of every (token, pair) angle it needs (one angle per pair when the
+// rotation is the same for every token) and keeps them in LDS as fp32 head + tail pairs; each
+// thread then streams 16-byte chunks of rows.  HBM-bound.
+#include "launch.h"
+#include "rope_math.h"
+
+namespace nexus {
+
+namespace {
+
+constexpr int kTileTokens = 8;        // tokens per workgroup
+constexpr int kLayersPerGroup = 16;   // layers per workgroup
+constexpr int kMaxPairsTab = 128;     // head_dim <= 256
+
+}  // namespace
+
+// Thread item = (chunk c of a row, row), rows ordered (layer, head, token) with the token of the
+// tile fastest; a tile always spans kTileTokens token slots and slots past n_tokens idle.
+// NEOX: chunk c covers pairs [N c, N c + N): elements [N c, +N) and [D/2 + N c, +N).
+// INTERLEAVED: elements [2 N c, 2 N c + 2 N) = pairs [N c, N c + N).
+template <typename T, bool INTERLEAVED, bool PER_TOKEN>
+__global__ __launch_bounds__(256) void rope_splice_kernel(
+    const T *__restrict__ src_k, const T *__restrict__ src_v, T *__restrict__ ck,
+    T *__restrict__ cv, const int32_t *__restrict__ map, int64_t offset, int32_t n_layers,
+    int32_t n_tokens, int32_t n_heads, FastDiv div_heads, int32_t head_dim, uint32_t tpr_shift,
+    int32_t n_phys_pages, int64_t angle0, double base) {
+  constexpr int N = Pack<T>::N;
+  constexpr int kBatch = 4;                       // items whose loads are in flight together
+  __shared__ float cs_tab[4][PER_TOKEN ? kTileTokens : 1][kMaxPairsTab];
+  const int j0 = blockIdx.x * kTileTokens;
+  const int l0 = blockIdx.y * kLayersPerGroup;
+  const int n_tok = min(kTileTokens, n_tokens - j0);
+  const int n_lay = min(kLayersPerGroup, n_layers - l0);
+  const int n_pairs = head_dim / 2;
+  const int n_ang = (PER_TOKEN ? n_tok : 1) * n_pairs;
+  for (int x = threadIdx.x; x < n_ang; x += blockDim.x) {
+    const int t = x / n_pairs, i = x - t * n_pairs;
+    // PER_TOKEN: token j0 + t sits at angle0 + j0 + t; otherwise every token turns by angle0
+    const int64_t d = PER_TOKEN ? angle0 + j0 + t : angle0;
+    pair_cs(d, base, i, head_dim, cs_tab[0][t][i], cs_tab[1][t][i], cs_tab[2][t][i],
+            cs_tab[3][t][i]);
+  }
+  __syncthreads();
+
+  const uint32_t items = (uint32_t)(n_lay * n_heads * kTileTokens) << tpr_shift;
+  const uint32_t tpr_mask = (1u << tpr_shift) - 1;
+  for (uint32_t it0 = threadIdx.x; it0 < items; it0 += kBatch * blockDim.x) {
+    u32x4 ka[kBatch], kb[kBatch], va[kBatch], vb[kBatch];
+    int64_t drow[kBatch];
+    int tt[kBatch], cc[kBatch];
+    bool ok[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const uint32_t it = it0 + u * blockDim.x;
+      const int c = it & tpr_mask;
+      const uint32_t r = it >> tpr_shift;
+      const int t = r % kTileTokens;
+      const uint32_t lh = r / kTileTokens;
+      const uint32_t lq = fdiv(lh, div_heads);
+      const int h = lh - lq * n_heads;
+      const int l = l0 + lq;
+      const int j = j0 + t;
+      ok[u] = it < items && t < n_tok;
+      tt[u] = PER_TOKEN ? t : 0;
+      cc[u] = c;
+      drow[u] = 0;
+      if (!ok[u]) continue;
+      const int64_t srow = (((int64_t)l * n_tokens + j) * n_heads + h) * head_dim;
+      const int64_t tok = offset + j;
+      const int64_t page = (uint32_t)map[tok >> kPageShift];
+      drow[u] = ((((int64_t)l * n_phys_pages + page) * n_heads + h) * kPage + (tok & (kPage - 1))) *
+                head_dim;
+      const int ea = INTERLEAVED ? 2 * N * c : N * c;            // first element of each load
+      const int eb = INTERLEAVED ? 2 * N * c + N : n_pairs + N * c;
+      ka[u] = *reinterpret_cast<const u32x4 *>(src_k + srow + ea);
+      kb[u] = *reinterpret_cast<const u32x4 *>(src_k + srow + eb);
+      if (src_v != nullptr) {
+        va[u] = *reinterpret_cast<const u32x4 *>(src_v + srow + ea);
+        vb[u] = *reinterpret_cast<const u32x4 *>(src_v + srow + eb);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      if (!ok[u]) continue;
+      const int c = cc[u];
+      const int ea = INTERLEAVED ? 2 * N * c : N * c;
+      const int eb = INTERLEAVED ? 2 * N * c + N : n_pairs + N * c;
+      float x[2 * N], a[N], b[N];
+      Pack<T>::unpack(ka[u], x);
+      Pack<T>::unpack(kb[u], x + N);
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        a[e] = INTERLEAVED ? x[2 * e] : x[e];
+        b[e] = INTERLEAVED ? x[2 * e + 1] : x[N + e];
+      }
+      float ch[N], cl[N], sh[N], sl[N];
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        ch[e] = cs_tab[0][tt[u]][N * c + e];
+        cl[e] = cs_tab[1][tt[u]][N * c + e];
+        sh[e] = cs_tab[2][tt[u]][N * c + e];
+        sl[e] = cs_tab[3][tt[u]][N * c + e];
+      }
+      rotate<N>(a, b, ch, cl, sh, sl);
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        if (INTERLEAVED) {
+          x[2 * e] = a[e];
+          x[2 * e + 1] = b[e];
+        } else {
+          x[e] = a[e];
+          x[N + e] = b[e];
+        }
+      }
+      *reinterpret_cast<u32x4 *>(ck + drow[u] + ea) = Pack<T>::pack(x);
+      *reinterpret_cast<u32x4 *>(ck + drow[u] + eb) = Pack<T>::pack(x + N);
+      if (src_v != nullptr) {
+        *reinterpret_cast<u32x4 *>(cv + drow[u] + ea) = va[u];
+        *reinterpret_cast<u32x4 *>(cv + drow[u] + eb) = vb[u];
+      }
+    }
+  }
+}
+
+hipError_t launch_rope_splice(const RopeSpliceLaunch &p, hipStream_t stream) {
+  // V of a transposed cache goes through the splice kernel's transposing path
+  const bool v_rows = !p.v_transposed;
+  const dim3 grid((p.n_tokens + kTileTokens - 1) / kTileTokens,
+                  (p.n_layers + kLayersPerGroup - 1) / kLayersPerGroup);
+  const uint32_t tpr = (uint32_t)(p.head_dim / 2 / (16 / p.dtype_bytes));
+  uint32_t shift = 0;
+  while ((1u << shift) < tpr) ++shift;
+  const FastDiv dh = make_fastdiv((uint32_t)p.n_heads);
+#define NEXUS_ROPE_SPLICE(T, IL, PT)                                                              \
+  hipLaunchKernelGGL((rope_splice_kernel<T, IL, PT>), grid, dim3(256), 0, stream,                \
+                     (const T *)p.src_k, v_rows ? (const T *)p.src_v : nullptr, (T *)p.cache_k,  \
+                     v_rows ? (T *)p.cache_v : nullptr, p.map, p.offset, p.n_layers, p.n_tokens, \
+                     p.n_heads, dh, p.head_dim, shift, p.n_phys_pages, p.angle0, p.rope_base)
+  if (p.dtype_bytes == 2) {
+    if (p.per_token) {
+      if (p.interleaved) NEXUS_ROPE_SPLICE(uint16_t, true, true);
+      else NEXUS_ROPE_SPLICE(uint16_t, false, true);
+    } else {
+      if (p.interleaved) NEXUS_ROPE_SPLICE(uint16_t, true, false);
+      else NEXUS_ROPE_SPLICE(uint16_t, false, false);
+    }
+  } else {
+    if (p.per_token) {
+      if (p.interleaved) NEXUS_ROPE_SPLICE(uint32_t, true, true);
+      else NEXUS_ROPE_SPLICE(uint32_t, false, true);
+    } else {
+      if (p.interleaved) NEXUS_ROPE_SPLICE(uint32_t, true, false);
+      else NEXUS_ROPE_SPLICE(uint32_t, false, false);
+    }
+  }
+#undef NEXUS_ROPE_SPLICE
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || v_rows) return e;
+  SpliceLaunch s{};
+  s.block_k = p.src_k;
+  s.block_v = p.src_v;
+  s.cache_k = p.cache_k;
+  s.cache_v = p.cache_v;
+  s.map = p.map;
+  s.offset = p.offset;
+  s.n_layers = p.n_layers;
+  s.n_tokens = p.n_tokens;
+  s.n_heads = p.n_heads;
+  s.head_dim = p.head_dim;
+  s.n_phys_pages = p.n_phys_pages;
+  s.dtype_bytes = p.dtype_bytes;
+  s.v_transposed = true;
+  s.v_only = true;
+  return launch_splice(s, stream);
+}
+
+}  // namespace nexus

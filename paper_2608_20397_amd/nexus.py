@@ -70,6 +70,8 @@ def lib():
         "nexus_rephase_k": (i32, [pB, i64, i64, f64, vp]),
         "nexus_rephase_k_paged": (i32, [pC, pT, i64, i32, i64, i64, f64, vp]),
         "nexus_splice_pages": (i32, [pC, pT, pB, i64, vp]),
+        "nexus_splice_rephase_pages": (i32, [pC, pT, pB, i64, i64, vp]),
+        "nexus_rope_append": (i32, [pC, pT, vp, vp, i32, i64, i64, vp]),
         "nexus_suffix_attn": (i32, [vp, i32, i32, pC, pT, i32, i64, f32, i32, f32, vp, vp, sz, vp]),
         "nexus_suffix_attn_workspace": (sz, [i32, i32, pC, i64]),
         "nexus_suffix_attn_varlen": (i32, [vp, i32, C.POINTER(C.c_int32), C.POINTER(C.c_int32),
@@ -162,6 +164,28 @@ def splice_pages(cache: PagedKVCache, block: Block, offset: int):
     cc, pt, cb = cache.c(), cache.pt(), block.c()
     _check(lib().nexus_splice_pages(C.byref(cc), C.byref(pt), C.byref(cb), offset, _stream()),
            "nexus_splice_pages")
+
+
+def splice_rephase_pages(cache: PagedKVCache, block: Block, offset: int, dst_pos: int):
+    """Splice ``block`` at ``offset`` with its keys re-anchored from block.base_pos to
+    ``dst_pos`` in the same pass (the block itself is left as it is)."""
+    cc, pt, cb = cache.c(), cache.pt(), block.c()
+    _check(lib().nexus_splice_rephase_pages(C.byref(cc), C.byref(pt), C.byref(cb), offset, dst_pos,
+                                            _stream()), "nexus_splice_rephase_pages")
+
+
+def rope_append(cache: PagedKVCache, k: torch.Tensor, v: torch.Tensor, offset: int, pos0: int):
+    """Write un-rotated keys ``k`` (rotated here to positions pos0 + j) and values ``v``, both
+    [L][T][H][D] of the cache dtype, into logical slots offset .. offset + T - 1."""
+    cc, pt = cache.c(), cache.pt()
+    L, T, H, D = k.shape
+    if tuple(v.shape) != (L, T, H, D) or not (k.is_contiguous() and v.is_contiguous()):
+        raise NexusError(ESHAPE, "k/v must be contiguous [L][T][H][D] of equal shape")
+    if (L, H, D) != (cc.n_layers, cc.n_kv_heads, cc.head_dim) or _dtype_code(k) != cc.dtype \
+            or _dtype_code(v) != cc.dtype:
+        raise NexusError(ESHAPE, "k/v must match the cache's layers, heads, head_dim and dtype")
+    _check(lib().nexus_rope_append(C.byref(cc), C.byref(pt), _ptr(k), _ptr(v), T, offset, pos0,
+                                   _stream()), "nexus_rope_append")
 
 
 def rephase_k(block: Block, src_pos: int, dst_pos: int, rope_base: float):

@@ -54,10 +54,11 @@ def _dev(x, wl, dev):
     return x if isinstance(x, torch.Tensor) else G.bits_to_torch(x, wl.dtype, dev)
 
 
-def gpu_build_cache(hc, n_phys_pages=None, page_map=None, dev="cuda"):
+def gpu_build_cache(hc, n_phys_pages=None, page_map=None, dev="cuda", fused=False):
     """Device cache after context + blocks (+ re-anchor) + user tokens, through the library.
 
-    ``hc`` holds raw host bits (``synth.gen.HostCase``) or device tensors (``DeviceCase``)."""
+    ``hc`` holds raw host bits (``synth.gen.HostCase``) or device tensors (``DeviceCase``).
+    ``fused`` splices and re-anchors each block in one call (nexus_splice_rephase_pages)."""
     wl = hc.wl
     L = hc.ctx_k.shape[0]
     pm = hc.page_map if page_map is None else page_map
@@ -66,8 +67,12 @@ def gpu_build_cache(hc, n_phys_pages=None, page_map=None, dev="cuda"):
     if hc.n_ctx:
         N.splice_pages(cache, N.Block(t(hc.ctx_k), t(hc.ctx_v), 0, wl.rope_base), 0)
     for b, pos in enumerate(wl.splice_pos):
-        N.splice_pages(cache, N.Block(t(hc.blk_k[b]), t(hc.blk_v[b]), wl.anchor, wl.rope_base), pos)
-        N.rephase_k_paged(cache, pos, wl.block_len, wl.anchor, pos, wl.rope_base)
+        blk = N.Block(t(hc.blk_k[b]), t(hc.blk_v[b]), wl.anchor, wl.rope_base)
+        if fused:
+            N.splice_rephase_pages(cache, blk, pos, pos)
+        else:
+            N.splice_pages(cache, blk, pos)
+            N.rephase_k_paged(cache, pos, wl.block_len, wl.anchor, pos, wl.rope_base)
     if wl.n_user:
         u0 = user_offset(wl)
         N.splice_pages(cache, N.Block(t(hc.user_k), t(hc.user_v), u0, wl.rope_base), u0)
@@ -208,3 +213,30 @@ def compare(got: np.ndarray, ref: np.ndarray):
 
 BF16_MAX_ABS, BF16_REL_RMS = 2e-2, 5e-3      # bf16 attention outputs
 F32_TOL = 1e-5                               # fp32 re-phased keys and fp32 attention outputs
+
+
+# ------------------------------------------------------------------ key comparisons
+def range_mask(wl, L, n_phys_pages, page_map):
+    """Boolean K-cache mask of the re-anchored block rows, by oracle addressing."""
+    shape = (L, n_phys_pages, wl.n_kv_heads, PAGE, wl.head_dim)
+    m = np.zeros(shape, bool)
+    for pos in wl.splice_pos:
+        for t in range(pos, pos + wl.block_len):
+            m[:, page_map[t // PAGE], :, t % PAGE, :] = True
+    return m
+
+
+def check_keys(gk, ok, mask, dtype, tag):
+    assert np.array_equal(gk[~mask], ok[~mask]), f"{tag}: bits outside the re-anchored rows"
+    if dtype == "bf16":
+        a = O.bf16_bits_to_f64(gk[mask])
+        b = O.bf16_bits_to_f64(ok[mask])
+        ulp = np.abs(b) * 2.0 ** -7
+        ulp = np.maximum(ulp, 2.0 ** -133)
+        assert np.all(np.abs(a - b) <= ulp + 1e-300), f"{tag}: more than 1 ulp"
+        exact = np.mean(gk[mask] == ok[mask])
+        assert exact >= 0.999, f"{tag}: only {exact:.5f} exactly rounded"
+    else:
+        a = gk[mask].view(np.float32).astype(np.float64)
+        b = ok[mask].view(np.float32).astype(np.float64)
+        assert np.max(np.abs(a - b)) <= 1e-5, f"{tag}: f32 keys off by {np.max(np.abs(a - b))}"

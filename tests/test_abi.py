@@ -140,6 +140,38 @@ def test_rephase_validation_and_identity():
     assert L.nexus_rephase_k_paged(C.byref(cache), C.byref(pt), 0, 20, 0, 7, 2e4, s) == N.EROPE
 
 
+def test_fused_splice_and_rope_append_validation_fails_closed():
+    L = N.lib()
+    buf, cache, block, pt = _setup()
+    s = C.c_void_p(0)
+    f = L.nexus_splice_rephase_pages
+    # the splice checks apply unchanged
+    assert f(None, C.byref(pt), C.byref(block), 0, 5, s) == N.EINVAL
+    bad = N.CBlock.from_buffer_copy(block); bad.rope_base = 1e6
+    assert f(C.byref(cache), C.byref(pt), C.byref(bad), 0, 5, s) == N.EROPE
+    bad = N.CBlock.from_buffer_copy(block); bad.n_kv_heads = 1
+    assert f(C.byref(cache), C.byref(pt), C.byref(bad), 0, 5, s) == N.ESHAPE
+    bad = N.CBlock.from_buffer_copy(block); bad.dtype = N.F32
+    assert f(C.byref(cache), C.byref(pt), C.byref(bad), 0, 5, s) == N.EDTYPE
+    assert f(C.byref(cache), C.byref(pt), C.byref(block), 77, 5, s) == N.ERANGE
+    assert f(C.byref(cache), C.byref(pt), C.byref(block), 0, -1, s) == N.ERANGE
+    buf2, big, bigblk, pt2 = _setup(D=512)
+    assert f(C.byref(big), C.byref(pt2), C.byref(bigblk), 0, 5, s) == N.ESHAPE
+    assert block.base_pos == 0                          # the block is never re-anchored
+    g = L.nexus_rope_append
+    k, v = buf(2 * 20 * 2 * 64 * 2), buf(2 * 20 * 2 * 64 * 2)
+    assert g(None, C.byref(pt), k, v, 20, 0, 0, s) == N.EINVAL
+    assert g(C.byref(cache), C.byref(pt), None, v, 20, 0, 0, s) == N.EINVAL
+    assert g(C.byref(cache), C.byref(pt), k, None, 20, 0, 0, s) == N.EINVAL
+    assert g(C.byref(cache), C.byref(pt), k, v, 0, 0, 0, s) == N.EINVAL
+    assert g(C.byref(cache), C.byref(pt), k, v, 20, -1, 0, s) == N.ERANGE
+    assert g(C.byref(cache), C.byref(pt), k, v, 20, 0, -1, s) == N.ERANGE
+    assert g(C.byref(cache), C.byref(pt), k, v, 20, 77, 0, s) == N.ERANGE
+    assert g(C.byref(big), C.byref(pt2), k, v, 20, 0, 0, s) == N.ESHAPE
+    bc = N.CKvCache.from_buffer_copy(cache); bc.page_size = 32
+    assert g(C.byref(bc), C.byref(pt), k, v, 20, 0, 0, s) == N.ESHAPE
+
+
 def test_attention_validation_fails_closed():
     L = N.lib()
     buf, cache, block, pt = _setup(D=128)

@@ -18,35 +18,9 @@ from paper_2608_20397_amd import nexus as N
 from synth import PAGE
 from synth import gen as G
 
-from _pipeline import VL, gpu_build_cache, oracle_cache
+from _pipeline import VL, check_keys, gpu_build_cache, oracle_cache, range_mask
 
 pytestmark = pytest.mark.gpu
-
-
-def _range_mask(wl, L, n_phys_pages, page_map):
-    """Boolean K-cache mask of the re-anchored block rows, by oracle addressing."""
-    shape = (L, n_phys_pages, wl.n_kv_heads, PAGE, wl.head_dim)
-    m = np.zeros(shape, bool)
-    for pos in wl.splice_pos:
-        for t in range(pos, pos + wl.block_len):
-            m[:, page_map[t // PAGE], :, t % PAGE, :] = True
-    return m
-
-
-def _check_keys(gk, ok, mask, dtype, tag):
-    assert np.array_equal(gk[~mask], ok[~mask]), f"{tag}: bits outside the re-anchored rows"
-    if dtype == "bf16":
-        a = O.bf16_bits_to_f64(gk[mask])
-        b = O.bf16_bits_to_f64(ok[mask])
-        ulp = np.abs(b) * 2.0 ** -7
-        ulp = np.maximum(ulp, 2.0 ** -133)
-        assert np.all(np.abs(a - b) <= ulp + 1e-300), f"{tag}: more than 1 ulp"
-        exact = np.mean(gk[mask] == ok[mask])
-        assert exact >= 0.999, f"{tag}: only {exact:.5f} exactly rounded"
-    else:
-        a = gk[mask].view(np.float32).astype(np.float64)
-        b = ok[mask].view(np.float32).astype(np.float64)
-        assert np.max(np.abs(a - b)) <= 1e-5, f"{tag}: f32 keys off by {np.max(np.abs(a - b))}"
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 4, 5])
@@ -60,8 +34,8 @@ def test_splice_rephase_cache_parity(cfg):
     ck, cv = oracle_cache(hc, n_phys_pages=npp)
     gk, gv = G.torch_to_bits(cache.k), G.torch_to_bits(cache.v)
     assert np.array_equal(gv, cv), "V cache bits differ"
-    mask = _range_mask(wl, 1, npp, hc.page_map)
-    _check_keys(gk, ck, mask, wl.dtype, f"cfg{cfg}")
+    mask = range_mask(wl, 1, npp, hc.page_map)
+    check_keys(gk, ck, mask, wl.dtype, f"cfg{cfg}")
     # the unmapped physical pages still hold the sentinel
     s = G.SENTINEL[wl.dtype]
     unmapped = sorted(set(range(npp)) - set(hc.page_map.tolist()))
@@ -108,7 +82,7 @@ def test_rephase_block_contiguous(dtype, style, D, base):
         assert blk.base_pos == dst
         ref = O.round_to_storage(O.rephase(O.storage_to_f64(ref, dtype), src, dst, base, st), dtype)
         if dst == 32767:
-            _check_keys(G.torch_to_bits(k), ref, np.ones(bits.shape, bool), dtype, f"{dtype} {style}")
+            check_keys(G.torch_to_bits(k), ref, np.ones(bits.shape, bool), dtype, f"{dtype} {style}")
     # after two roundings the chains may part by the first step's rare 1-ulp differences
     got = O.storage_to_f64(G.torch_to_bits(k), dtype)
     want = O.storage_to_f64(ref, dtype)
