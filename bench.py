@@ -268,6 +268,100 @@ def time_next_rows(S, reps: int):
     return out
 
 
+SWEEP_DEPTHS = (256, 512, 1024, 2048, 4096, 16384)
+
+
+def sweep(reps: int):
+    """Depth-adaptive sweep (the shape of Table tab:perf without weights): attention time of a full
+    prefill against the splice path, all 48 layers of Qwen2.5-14B attention shapes, a 512-token
+    block and 64 user tokens at context depth n_past.  Prefill = causal attention of all
+    n_past + 512 + 64 tokens.  Splice path = prefill of the n_past context tokens, the one-pass
+    splice + re-anchor of the block (all layers) and the attention of the redecoded
+    r = redecode_len(512, n_past, 256, 5, K) block tokens plus the user tokens over the whole
+    cache.  Each variant's 48-layer call sequence is captured in a HIP graph and replayed, so
+    host launch overhead does not enter the comparison."""
+    import torch
+    from paper_2608_20397_amd import nexus as N
+    from synth import PAGE
+    from synth import gen as G
+    L, Hq, H, D, S, u, base, cfg = 48, 40, 8, 128, 512, 64, 1e6, 2
+    M, r_base = 256, 5
+    std = 128 ** -0.5
+
+    def graph_ms(calls):
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            calls()                                   # warm-up outside the capture
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            calls()
+        g.replay()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(max(reps, 5)):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            g.replay()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        ts.sort()
+        return ts[len(ts) // 2]
+
+    rows = []
+    for n_past in SWEEP_DEPTHS:
+        total = n_past + S + u
+        npp = (total + PAGE - 1) // PAGE
+        k = G.device_normal(cfg, n_past, G.TAG["k_ctx"], (L, npp, H, PAGE, D), std, "bf16", "cuda")
+        v = G.device_normal(cfg, n_past, G.TAG["v_ctx"], (L, npp, H, PAGE, D), std, "bf16", "cuda")
+        cache = N.PagedKVCache(k, v, torch.arange(npp, dtype=torch.int32, device="cuda"), base)
+        blk = N.Block(G.device_normal(cfg, n_past, G.TAG["k_blk"], (L, S, H, D), std, "bf16", "cuda"),
+                      G.device_normal(cfg, n_past, G.TAG["v_blk"], (L, S, H, D), std, "bf16", "cuda"),
+                      0, base)
+        q = G.device_normal(cfg, n_past, G.TAG["q"], (L, total, Hq, D), std, "bf16", "cuda")
+
+        def attn_calls(r0, r1, n0):
+            qs = [q[l, r0:r1].contiguous() for l in range(L)]
+            outs = [torch.empty_like(x) for x in qs]
+            ws = torch.empty(max(N.suffix_attn_workspace_bytes(cache, r1 - r0, Hq, n0), 16),
+                             dtype=torch.uint8, device="cuda")
+
+            def run():
+                for l in range(L):
+                    N.suffix_attn(qs[l], cache, l, n0, 0.0, out=outs[l], workspace=ws)
+            return run
+
+        prefill = attn_calls(0, total, 0)
+        context = attn_calls(0, n_past, 0)
+        t_prefill = graph_ms(prefill)
+        t_splice = graph_ms(lambda: N.splice_rephase_pages(cache, blk, n_past, n_past))
+        t_ctx = graph_ms(context)
+        for K in (4, 16):
+            r = N.redecode_len(S, n_past, M, r_base, K)
+            n_s = r + u
+            suffix = attn_calls(total - n_s, total, total - n_s)
+
+            def path():
+                context()
+                N.splice_rephase_pages(cache, blk, n_past, n_past)
+                suffix()
+            t_suf = graph_ms(suffix)
+            t_path = graph_ms(path)
+            R = r_base if n_past <= M else min(
+                100.0, r_base + (n_past - M) * (100.0 - r_base) / (M * (K - 1)))
+            rows.append({"K": K, "n_past": n_past, "R_pct": round(R, 1), "redecode": r,
+                         "prefill_ms": t_prefill, "context_ms": t_ctx, "splice_ms": t_splice,
+                         "suffix_ms": t_suf, "splice_path_ms": t_path,
+                         "speedup": t_prefill / t_path,
+                         "query_tokens_ratio": total / (n_past + n_s)})
+        del k, v, cache, blk, q
+        torch.cuda.empty_cache()
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -278,6 +372,9 @@ def main():
                     help="KV heads per layer the oracle baseline computes (0 skips it)")
     ap.add_argument("--cpu-layers", type=int, default=3,
                     help="layers the oracle baseline computes")
+    ap.add_argument("--sweep", action="store_true",
+                    help="only run the depth-adaptive sweep (attention-only prefill vs splice "
+                         "path over context depths, K = 4 and 16), print it as JSON, then exit")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only time a plain device copy of MIB MiB (HBM reference and the "
                          "scale of the FETCH_SIZE / WRITE_SIZE counters), then exit")
@@ -309,6 +406,11 @@ def main():
     from paper_2608_20397_amd import nexus as N
     N.lib()   # fail loudly if the library is not built
     torch.cuda.set_device(0)
+    if args.sweep:
+        print(json.dumps({"sweep": sweep(args.steps), "unit": "ms for all 48 layers",
+                          "shapes": "Qwen2.5-14B attention (40/8/128, theta 1e6), block 512, "
+                                    "user 64, bf16, 48 layers, HIP-graph replay"}), flush=True)
+        return
     S = setup(args.config)
     wl = S["wl"]
     print(f"bench: cfg{wl.cfg} {wl.name}: setup done", file=sys.stderr, flush=True)

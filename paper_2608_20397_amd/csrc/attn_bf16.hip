@@ -27,6 +27,7 @@
 #include <stdlib.h>
 
 #include <algorithm>
+#include <vector>
 
 namespace nexus {
 
@@ -56,7 +57,10 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
   const SeqPlan sp = plan.seq[b];
   unit -= sp.first_unit;
   const int split = unit % sp.n_splits;
-  const int tgrp = unit / sp.n_splits;
+  // prefill-like sequences take their task groups in reverse: later queries see more keys, so
+  // the longest workgroups are dispatched first and the launch does not end on them
+  const int tgrp = sp.longest_first ? (sp.n_tasks + kWaves - 1) / kWaves - 1 - unit / sp.n_splits
+                                    : unit / sp.n_splits;
   const int G = a.group;
 
   const int task = tgrp * kWaves + wave;
@@ -405,23 +409,47 @@ constexpr int kCUs = 256;
 
 // Deterministic plan of an attention launch: task groups, key splits and workspace offsets.
 // The same arguments always give the same plan (the workspace query relies on it).
-// The split length is chosen to minimise the critical path, modelled as (rounds of resident
-// workgroups) x (keys per workgroup), with a small charge per extra split for the partials.
+// The split length is chosen to minimise an estimate of the launch time: the critical path over
+// the resident workgroup slots (the longest piece of work, the total work spread over the slots,
+// and the rounds that the near-full-length pieces need: uniform suffix shapes are decided by the
+// the latter, causal prefills by the former two) at about 0.03 us per key per workgroup for
+// head_dim 128 (measured), plus, when keys are split, the combine: writing and reading the fp32
+// partials at about 4 TB/s and one more launch.  A piece's work is its keys plus a fixed 128 for
+// its prologue and epilogue.
 bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   if (p.n_seqs < 1 || p.n_seqs > kMaxSeqs) return false;
   const int G = p.n_q_heads / p.n_kv_heads;
   const KernelShape ks = kernel_shape(p);
   const int KT = ks.key_tile;
   const int64_t slots = (int64_t)kCUs * ks.wgs_per_cu;
+  constexpr int64_t kPieceOverhead = 128;
   plan = AttnPlan{};
   plan.n_seqs = p.n_seqs;
   int64_t max_keys = 0;
   for (int b = 0; b < p.n_seqs; ++b)
     max_keys = std::max<int64_t>(max_keys, p.seqs[b].n_past + p.seqs[b].len);
-  auto n_tg_of = [&](const AttnSeq &s) {
-    const int n_tasks = G * ((s.len + ks.qpw - 1) / ks.qpw);
-    return (int64_t)((n_tasks + kWaves - 1) / kWaves);
+  auto n_tasks_of = [&](const AttnSeq &s) { return G * ((s.len + ks.qpw - 1) / ks.qpw); };
+  // split length of a sequence for a global candidate: equal key counts rounded to the tile
+  auto seq_split = [&](int64_t keys, int64_t sk) {
+    int64_t ns = (keys + sk - 1) / sk;
+    if (ns < 1) ns = 1;
+    int64_t skb = (keys + ns - 1) / ns;
+    return (skb + KT - 1) / KT * KT;
   };
+  // keys of each task group (nondecreasing in the group index), once per sequence
+  std::vector<std::vector<int64_t>> tg_keys(p.n_seqs);
+  std::vector<double> seq_keys(p.n_seqs, 0.0);
+  for (int b = 0; b < p.n_seqs; ++b) {
+    const AttnSeq &s = p.seqs[b];
+    const int n_tasks = n_tasks_of(s);
+    const int n_tg = (n_tasks + kWaves - 1) / kWaves;
+    tg_keys[b].resize(n_tg);
+    for (int tg = 0; tg < n_tg; ++tg) {
+      const int last_task = std::min(tg * kWaves + kWaves - 1, n_tasks - 1);
+      tg_keys[b][tg] = s.n_past + std::min((last_task / G + 1) * ks.qpw, s.len);
+      seq_keys[b] += (double)tg_keys[b][tg];
+    }
+  }
   int64_t best_sk = kMaxSplitKeys;
   double best_cost = 1e300;
   for (int ns = 1; ns <= 64; ++ns) {
@@ -429,16 +457,45 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     sk = (sk + KT - 1) / KT * KT;
     if (sk > kMaxSplitKeys) continue;
     if (sk < 512 && ns > 1) break;
-    int64_t wgs = 0, max_splits = 1;
+    int64_t max_splits = 1, n_full = 0, full_len = 0, max_piece = 0;
+    double total = 0.0, combine_bytes = 0.0;
     for (int b = 0; b < p.n_seqs; ++b) {
-      const int64_t keys = p.seqs[b].n_past + p.seqs[b].len;
-      const int64_t nsb = (keys + sk - 1) / sk;
+      const AttnSeq &s = p.seqs[b];
+      const std::vector<int64_t> &wk = tg_keys[b];
+      const int64_t keys = s.n_past + s.len;
+      const int64_t skb = seq_split(keys, sk);
+      const int64_t nsb = (keys + skb - 1) / skb;
       max_splits = std::max(max_splits, nsb);
-      wgs += n_tg_of(p.seqs[b]) * nsb;
+      if (nsb > 1)
+        combine_bytes += 8.0 * nsb * s.len * p.n_q_heads * (p.head_dim + 2) +
+                         2.0 * s.len * p.n_q_heads * p.head_dim;
+      // piece j of a task group is non-empty when its keys exceed j * skb, and counts as
+      // full-length for the rounds when it holds at least half the split length.  Suffix-like
+      // sequences (all task groups within 10% of the same keys) take the closed form.
+      int64_t pieces = 0, full = 0;
+      if (!wk.empty() && wk.front() * 10 >= wk.back() * 9) {
+        const int64_t n_tg = (int64_t)wk.size();
+        pieces = n_tg * nsb;
+        full = n_tg * (nsb - 1) + (2 * (wk.back() - (nsb - 1) * skb) >= skb ? n_tg : 0);
+        if (full > 0) full_len = std::max(full_len, skb);
+      } else {
+        for (int64_t jp = 0; jp < nsb; ++jp) {
+          pieces += wk.end() - std::upper_bound(wk.begin(), wk.end(), jp * skb);
+          const int64_t f =
+              wk.end() - std::lower_bound(wk.begin(), wk.end(), jp * skb + (skb + 1) / 2);
+          full += f;
+          if (f > 0) full_len = std::max(full_len, skb);
+        }
+      }
+      n_full += full * p.n_kv_heads;
+      if (!wk.empty()) max_piece = std::max(max_piece, std::min(skb, wk.back()) + kPieceOverhead);
+      total += (seq_keys[b] + (double)pieces * kPieceOverhead) * p.n_kv_heads;
     }
-    wgs *= p.n_kv_heads;
-    const double rounds = (double)((wgs + slots - 1) / slots);
-    const double cost = rounds * (double)std::min(sk, max_keys) * (1.0 + 0.03 * (max_splits - 1));
+    const double rounds_full = (double)((n_full + slots - 1) / slots);
+    const double est = std::max({rounds_full * (double)(full_len + kPieceOverhead),
+                                 (double)max_piece, total / (double)slots});
+    const double cost = est * 0.03 * p.head_dim / 128.0 +
+                        (max_splits > 1 ? combine_bytes / 4.0e6 + 8.0 : 0.0);
     if (cost < best_cost - 1e-9) {
       best_cost = cost;
       best_sk = sk;
@@ -466,6 +523,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     ns = (keys + sk - 1) / sk;
     sp.n_splits = (int32_t)ns;
     sp.split_keys = (int32_t)sk;
+    sp.longest_first = s.n_past < s.len ? 1 : 0;
     unit += n_tg * sp.n_splits;
     rows += s.len;
     if (sp.n_splits > 1) {

@@ -105,7 +105,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
   const SeqPlan sp = plan.seq[b];
   unit -= sp.first_unit;
   const int split = unit % sp.n_splits;
-  const int tgrp = unit / sp.n_splits;
+  // prefill-like sequences take their task groups in reverse: later queries see more keys, so
+  // the longest workgroups are dispatched first and the launch does not end on them
+  const int tgrp = sp.longest_first ? (sp.n_tasks + kWaves - 1) / kWaves - 1 - unit / sp.n_splits
+                                    : unit / sp.n_splits;
   const int G = a.group;
 
   const int task = tgrp * kWaves + wave;

@@ -8,7 +8,7 @@ namespace nexus {
 constexpr int kMaxSeqs = 32;
 constexpr int kWaves = 4;
 constexpr int kQB = 32;   // queries per wave task
-constexpr int kMaxSplitKeys = 16384;   // keys one workgroup covers at most
+constexpr int kMaxSplitKeys = 32768;   // keys one workgroup covers at most (LDS page table)
 
 struct SeqPlan {
   int32_t q_start;     // first row of q / out
@@ -19,7 +19,7 @@ struct SeqPlan {
   int32_t n_tasks;     // group * ceil(len / 32)
   int32_t n_splits;
   int32_t split_keys;  // keys per split, a multiple of the key tile
-  int32_t pad_;
+  int32_t longest_first;  // dispatch task groups last-first (causal prefill: n_past < len)
   int64_t ws_off;      // float offset of the partial O of this sequence in the workspace
   int64_t ml_off;      // float offset of its (m, l) pairs
 };
