@@ -235,17 +235,18 @@ def time_next_rows(S, reps: int):
     L, H, D = wl.n_layers, wl.n_kv_heads, wl.head_dim
 
     def timeit(fn):
+        # back-to-back calls between two events on the launch stream: kernel time, not the
+        # host's launch latency of a lone call
         fn()
         torch.cuda.synchronize()
-        ts = []
-        for _ in range(max(reps, 3)):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
+        n = max(reps, 3)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(n):
             fn()
-            b.record()
-            torch.cuda.synchronize()
-            ts.append(a.elapsed_time(b))
-        return sum(ts) / len(ts)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
 
     out = {}
     blk_bytes = L * wl.block_len * H * D * esize
