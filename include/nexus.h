@@ -218,6 +218,42 @@ size_t nexus_suffix_attn_varlen_workspace(int32_t n_seqs, const int32_t *q_start
                                           int32_t n_q_heads, const nexus_kv_cache *cache);
 
 /*
+ * Decode-step attention: one new query token per sequence over the paged cache (the token-by-
+ * token generation that follows the spliced prefill; scaled dot-product attention of Sec. III-A,
+ * soft-cap and transposed V per Sec. VI-B).  Each sequence has its own page map, and sequences
+ * may share physical pages (a warm prefix).
+ *   q           [n_seqs][n_q_heads][head_dim] of the cache dtype, already rotated; the query of
+ *               sequence b sits at position seq_len[b] - 1 and its own key and value must
+ *               already be in the cache (nexus_rope_append).
+ *   maps        DEVICE int32 [n_seqs][map_stride]: logical page p of sequence b is physical page
+ *               maps[b * map_stride + p].  Entries of pages below ceil(seq_len[b] / 16) must be
+ *               in [0, n_phys_pages); they are not checked.
+ *   seq_len     DEVICE int32 [n_seqs]: cached tokens of each sequence (the query attends to all
+ *               of them).  Values are clamped to [0, max_seq_len]; a sequence of length 0 gets a
+ *               zero output row.  Living on the device, the lengths can advance between replays
+ *               of one captured launch.
+ *   max_seq_len host upper bound of seq_len, 0 <= max_seq_len <= 16 * map_stride (NEXUS_ERANGE).
+ *               It fixes the launch shape: keys are cut into splits of a fixed number of pages
+ *               chosen from n_seqs, the head counts and max_seq_len, merged by a second kernel.
+ *   layer, softcap, v_layout, scale: as nexus_suffix_attn (same checks, same head_dim limits).
+ *   out         [n_seqs][n_q_heads][head_dim] of the cache dtype.
+ *   workspace   at least nexus_decode_attn_workspace() bytes (NULL allowed when that is 0);
+ *               contents on entry do not matter.
+ * bf16 caches: each workgroup reads a KV head's keys and values once for up to 16 query heads
+ * (MFMA, fp32 accumulation, probabilities rounded to bf16 as in nexus_suffix_attn).  f32 caches:
+ * fp32 VALU kernel.
+ */
+nexus_status nexus_decode_attn(const void *q, int32_t n_seqs, int32_t n_q_heads,
+                               const nexus_kv_cache *cache, const int32_t *maps,
+                               int32_t map_stride, const int32_t *seq_len, int32_t max_seq_len,
+                               int32_t layer, float softcap, int32_t v_layout, float scale,
+                               void *out, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Workspace bytes nexus_decode_attn needs (0 if none, SIZE_MAX if the arguments are invalid). */
+size_t nexus_decode_attn_workspace(int32_t n_seqs, int32_t n_q_heads, const nexus_kv_cache *cache,
+                                   int32_t max_seq_len);
+
+/*
  * Redecode length of eq. (adaptive): ceil(S * R(n_past) / 100) with R = r_base for n_past <= M
  * and R = r_base + (n_past - M) / (M (K - 1)) * (100 - r_base) above, clamped to 100 (Sec. III-C;
  * the suffix length of Sec. VI-A).  Exact integer arithmetic.  Host only; returns -1 unless

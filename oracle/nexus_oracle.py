@@ -16,6 +16,7 @@ What it computes (paper sections cited per function):
 * Causal grouped-query scaled dot-product attention softmax(QK^T/sqrt(d))V (Sec. III-A) for the
   re-decoded suffix, with optional Gemma-2-style tanh logit soft-capping (Sec. VI-B names the
   soft-capped model family).  Full rows, two-pass softmax.
+* The decode step that follows: one query per sequence over that sequence's own page map.
 * The depth-adaptive recompute fraction R(n_past) of eq. (adaptive) and the redecode length
   ceil(S * R / 100) of Sec. VI-A, in exact rational arithmetic.
 * Round-to-nearest-even from fp64 to bfloat16, used to round re-phased keys back to the
@@ -297,6 +298,33 @@ def suffix_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, n_past: int,
         if return_probs:
             probs[h] = p
     return (out, probs) if return_probs else out
+
+
+def decode_attention(q: np.ndarray, cache_k: np.ndarray, cache_v: np.ndarray,
+                     page_maps: np.ndarray, seq_lens, page_size: int,
+                     v_layout: str = ROWMAJOR, scale: float | None = None,
+                     softcap: float = 0.0) -> np.ndarray:
+    """One decode step per sequence over its own pages (Sec. III-A attention, one query).
+
+    * ``q``: [B][H_q][D] values; the query of sequence b sits at position seq_lens[b] - 1.
+    * ``cache_k`` / ``cache_v``: ONE layer of a paged cache as values, [n_phys_pages][H_kv][P][D]
+      (V transposed: [H_kv][D][n_phys_pages * P]).
+    * ``page_maps``: [B][stride], logical page p of sequence b -> physical page.
+
+    The step is the suffix attention of a single query whose keys are the sequence's cached
+    tokens 0 .. seq_lens[b] - 1, its own included: gather them through the sequence's map and
+    call ``suffix_attention`` with n_past = seq_lens[b] - 1.  A sequence with no cached token
+    gets a zero row.  Returns [B][H_q][D] fp64.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    out = np.zeros(q.shape, dtype=np.float64)
+    for b, n in enumerate(seq_lens):
+        n = int(n)
+        if n == 0:
+            continue
+        k, v = gather_logical(cache_k[None], cache_v[None], page_maps[b], n, page_size, v_layout)
+        out[b] = suffix_attention(q[b:b + 1], k[0], v[0], n - 1, scale, softcap)[0]
+    return out
 
 
 # --------------------------------------------------------------------------------------

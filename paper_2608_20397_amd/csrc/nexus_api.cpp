@@ -421,4 +421,89 @@ nexus_status nexus_suffix_attn_varlen(const void *q, int32_t n_seqs, const int32
   return run_attention(L, workspace, workspace_bytes, stream);
 }
 
+namespace {
+
+// Checks of the decode entry point; fills `L` (without the workspace) on success.
+nexus_status prepare_decode(const void *q, int32_t n_seqs, int32_t n_q_heads,
+                            const nexus_kv_cache *cache, const int32_t *maps, int32_t map_stride,
+                            const int32_t *seq_len, int32_t max_seq_len, int32_t layer,
+                            float softcap, int32_t v_layout, float scale, void *out,
+                            DecodeLaunch &L) {
+  nexus_status st = check_cache(cache);
+  if (st) return st;
+  if (!q || !out || !maps || !seq_len || n_seqs <= 0 || map_stride <= 0) return NEXUS_EINVAL;
+  if (!valid_layout(v_layout)) return NEXUS_EINVAL;
+  if (v_layout != cache->v_layout) return NEXUS_ELAYOUT;
+  if (layer < 0 || layer >= cache->n_layers) return NEXUS_ERANGE;
+  if (max_seq_len < 0 || (int64_t)map_stride * kPageSize < max_seq_len) return NEXUS_ERANGE;
+  if (n_q_heads <= 0 || n_q_heads % cache->n_kv_heads) return NEXUS_ESHAPE;
+  if (!(softcap >= 0.f) || !isfinite(softcap)) return NEXUS_EINVAL;
+  if (!(scale >= 0.f) || !isfinite(scale)) return NEXUS_EINVAL;
+  const bool bf16 = cache->dtype == NEXUS_BF16;
+  if (bf16) {
+    if (cache->head_dim != 64 && cache->head_dim != 128 && cache->head_dim != 256)
+      return NEXUS_ESHAPE;
+  } else if (cache->head_dim > 256) {
+    return NEXUS_ESHAPE;
+  }
+  // grid limits and 32-bit row offsets of q / out / the page maps
+  if (n_seqs > 65535 || n_q_heads > 65535) return NEXUS_ESHAPE;
+  if ((int64_t)n_seqs * n_q_heads * cache->head_dim >= kMaxElems32) return NEXUS_ESHAPE;
+  if ((int64_t)n_seqs * map_stride >= kMaxElems32) return NEXUS_ESHAPE;
+  L = DecodeLaunch{};
+  L.q = q;
+  L.out = out;
+  L.cache_k = cache->k;
+  L.cache_v = cache->v;
+  L.maps = maps;
+  L.lens = seq_len;
+  L.map_stride = map_stride;
+  L.max_len = max_seq_len;
+  L.layer = layer;
+  L.n_phys_pages = cache->n_phys_pages;
+  L.n_kv_heads = cache->n_kv_heads;
+  L.n_q_heads = n_q_heads;
+  L.head_dim = cache->head_dim;
+  L.n_seqs = n_seqs;
+  L.v_transposed = cache->v_layout == NEXUS_V_TRANSPOSED;
+  L.is_bf16 = bf16;
+  L.scale = scale > 0.f ? scale : 1.0f / sqrtf((float)cache->head_dim);
+  L.softcap = softcap;
+  return NEXUS_OK;
+}
+
+}  // namespace
+
+size_t nexus_decode_attn_workspace(int32_t n_seqs, int32_t n_q_heads, const nexus_kv_cache *cache,
+                                   int32_t max_seq_len) {
+  if (!cache || n_seqs <= 0 || max_seq_len < 0 || n_q_heads <= 0 || cache->n_kv_heads <= 0 ||
+      n_q_heads % cache->n_kv_heads || cache->head_dim <= 0)
+    return SIZE_MAX;
+  DecodeLaunch L{};
+  L.n_seqs = n_seqs;
+  L.n_q_heads = n_q_heads;
+  L.n_kv_heads = cache->n_kv_heads;
+  L.head_dim = cache->head_dim;
+  L.max_len = max_seq_len;
+  L.is_bf16 = cache->dtype == NEXUS_BF16;
+  return decode_workspace_bytes(L);
+}
+
+nexus_status nexus_decode_attn(const void *q, int32_t n_seqs, int32_t n_q_heads,
+                               const nexus_kv_cache *cache, const int32_t *maps,
+                               int32_t map_stride, const int32_t *seq_len, int32_t max_seq_len,
+                               int32_t layer, float softcap, int32_t v_layout, float scale,
+                               void *out, void *workspace, size_t workspace_bytes,
+                               void *stream) {
+  DecodeLaunch L;
+  nexus_status st = prepare_decode(q, n_seqs, n_q_heads, cache, maps, map_stride, seq_len,
+                                   max_seq_len, layer, softcap, v_layout, scale, out, L);
+  if (st) return st;
+  const size_t need = decode_workspace_bytes(L);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return NEXUS_EWORKSPACE;
+  L.workspace = workspace;
+  return from_hip(launch_decode(L, as_stream(stream)));
+}
+
+
 }  // extern "C"

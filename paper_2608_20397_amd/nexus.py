@@ -80,6 +80,9 @@ def lib():
         "nexus_suffix_attn_varlen_workspace": (sz, [i32, C.POINTER(C.c_int32),
                                                     C.POINTER(C.c_int32), C.POINTER(C.c_int64),
                                                     i32, pC]),
+        "nexus_decode_attn": (i32, [vp, i32, i32, pC, vp, i32, vp, i32, i32, f32, i32, f32, vp,
+                                    vp, sz, vp]),
+        "nexus_decode_attn_workspace": (sz, [i32, i32, pC, i32]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(L, name)
@@ -270,6 +273,51 @@ def suffix_attn_varlen(q: torch.Tensor, q_start, seq_len, seq_n_past, cache: Pag
                                           cache.v_layout if v_layout is None else v_layout,
                                           scale, _ptr(out), _ptr(ws), nbytes, _stream()),
            "nexus_suffix_attn_varlen")
+    return out
+
+
+def decode_attn_workspace_bytes(cache: PagedKVCache, n_seqs: int, n_q_heads: int,
+                                max_seq_len: int) -> int:
+    cc = cache.c()
+    n = lib().nexus_decode_attn_workspace(n_seqs, n_q_heads, C.byref(cc), max_seq_len)
+    if n == (1 << 64) - 1:
+        raise NexusError(EINVAL, "nexus_decode_attn_workspace")
+    return n
+
+
+def decode_attn(q: torch.Tensor, cache: PagedKVCache, maps: torch.Tensor, seq_len: torch.Tensor,
+                max_seq_len: int, layer: int, softcap: float = 0.0, v_layout: int | None = None,
+                scale: float = 0.0, out: torch.Tensor | None = None,
+                workspace: torch.Tensor | None = None):
+    """One query per sequence: q [n_seqs][n_q_heads][D] -> out (cache dtype).  ``maps`` is a
+    device int32 [n_seqs][map_stride] tensor of per-sequence page maps and ``seq_len`` a device
+    int32 [n_seqs] tensor (the cache's own page_map is not used)."""
+    n, hq, _ = q.shape
+    if not q.is_contiguous():
+        raise NexusError(EINVAL, "q must be contiguous")
+    if q.dtype != cache.k.dtype:
+        raise NexusError(EDTYPE, "q dtype differs from the cache")
+    if (maps.dtype != torch.int32 or maps.dim() != 2 or maps.shape[0] != n
+            or not maps.is_contiguous() or maps.device != q.device):
+        raise NexusError(EINVAL, "maps must be a contiguous int32 [n_seqs][stride] device tensor")
+    if (seq_len.dtype != torch.int32 or tuple(seq_len.shape) != (n,)
+            or not seq_len.is_contiguous() or seq_len.device != q.device):
+        raise NexusError(EINVAL, "seq_len must be a contiguous int32 [n_seqs] device tensor")
+    if out is None:
+        out = torch.empty_like(q)
+    elif out.shape != q.shape or out.dtype != q.dtype or not out.is_contiguous():
+        raise NexusError(EINVAL, "out must be contiguous, shaped and typed like q")
+    cc = cache.c()
+    ws_bytes = lib().nexus_decode_attn_workspace(n, hq, C.byref(cc), max_seq_len)
+    if ws_bytes == (1 << 64) - 1:
+        raise NexusError(EINVAL, "nexus_decode_attn_workspace")
+    ws = _workspace(ws_bytes, q.device, workspace)
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().nexus_decode_attn(_ptr(q), n, hq, C.byref(cc), _ptr(maps), maps.shape[1],
+                                   _ptr(seq_len), max_seq_len, layer, softcap,
+                                   cache.v_layout if v_layout is None else v_layout, scale,
+                                   _ptr(out), _ptr(ws), nbytes, _stream()),
+           "nexus_decode_attn")
     return out
 
 

@@ -223,6 +223,46 @@ def test_varlen_validation():
                                       0, 0.0, q, None, 0, s) == N.ERANGE          # 95 + 4 > 96
 
 
+def test_decode_validation_fails_closed():
+    L = N.lib()
+    buf, cache, block, pt = _setup(D=128)
+    s = C.c_void_p(0)
+    q, out = buf(3 * 4 * 128 * 2), buf(3 * 4 * 128 * 2)
+    maps, lens = buf(3 * 6 * 4), buf(3 * 4)
+    ok_args = lambda **kw: dict(dict(q=q, n=3, hq=4, maps=maps, stride=6, lens=lens, max_len=96,
+                                     layer=1, cap=0.0, vl=N.V_ROWMAJOR, scale=0.0, out=out), **kw)
+
+    def call(a, ws=None, wsb=0, cc=cache):
+        return L.nexus_decode_attn(a["q"], a["n"], a["hq"], C.byref(cc), a["maps"], a["stride"],
+                                   a["lens"], a["max_len"], a["layer"], a["cap"], a["vl"],
+                                   a["scale"], a["out"], ws, wsb, s)
+
+    assert call(ok_args(vl=N.V_TRANSPOSED)) == N.ELAYOUT
+    assert call(ok_args(vl=7)) == N.EINVAL
+    assert call(ok_args(hq=3)) == N.ESHAPE                  # 3 % 2 kv heads
+    assert call(ok_args(layer=2)) == N.ERANGE
+    assert call(ok_args(layer=-1)) == N.ERANGE
+    assert call(ok_args(max_len=97)) == N.ERANGE            # > 16 * stride
+    assert call(ok_args(max_len=-1)) == N.ERANGE
+    assert call(ok_args(n=0)) == N.EINVAL
+    assert call(ok_args(stride=0)) == N.EINVAL
+    assert call(ok_args(q=None)) == N.EINVAL
+    assert call(ok_args(maps=None)) == N.EINVAL
+    assert call(ok_args(lens=None)) == N.EINVAL
+    assert call(ok_args(out=None)) == N.EINVAL
+    assert call(ok_args(cap=-1.0)) == N.EINVAL
+    assert call(ok_args(scale=float("inf"))) == N.EINVAL
+    bc = N.CKvCache.from_buffer_copy(cache); bc.head_dim = 96
+    assert call(ok_args(), cc=bc) == N.ESHAPE
+    # a long bound needs a split workspace
+    need = L.nexus_decode_attn_workspace(3, 4, C.byref(cache), 96 * 64)
+    assert need > 0
+    assert call(ok_args(stride=6 * 64, max_len=96 * 64)) == N.EWORKSPACE
+    assert call(ok_args(stride=6 * 64, max_len=96 * 64), ws=buf(need), wsb=need - 1) == N.EWORKSPACE
+    assert L.nexus_decode_attn_workspace(3, 3, C.byref(cache), 96) == (1 << 64) - 1
+    assert L.nexus_decode_attn_workspace(0, 4, C.byref(cache), 96) == (1 << 64) - 1
+
+
 def test_status_strings():
     L = N.lib()
     for st in range(9):

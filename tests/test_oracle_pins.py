@@ -395,3 +395,94 @@ def test_rephase_paged_bits_rounds_only_the_range():
     l0, _ = O.gather_logical(ck, ck, perm, npg * P, P)
     assert np.array_equal(lk[:, :21], l0[:, :21]) and np.array_equal(lk[:, 51:], l0[:, 51:])
     assert np.array_equal(O.rephase_paged_bits(ck, "bf16", perm, P, 21, 30, 5, 5, 1e4), ck)
+
+
+# ---------------------------------------------------------------- decode step (one query per sequence)
+def _paged_values(rng, lens, hk, d, v_layout, shuffled=True, spare=2):
+    """A paged value cache holding every sequence's tokens on private pages, NaN elsewhere, plus
+    each sequence's logical K/V."""
+    P = 16
+    npg = [-(-n // P) for n in lens]
+    n_phys = sum(npg) + spare
+    order = rng.permutation(n_phys) if shuffled else np.arange(n_phys)
+    maps = np.full((len(lens), max(1, max(npg))), -1, np.int64)
+    ck = np.full((n_phys, hk, P, d), np.nan)
+    cv = np.full((n_phys, hk, P, d), np.nan)
+    logical = []
+    nxt = 0
+    for b, n in enumerate(lens):
+        k = rng.standard_normal((n, hk, d))
+        v = rng.standard_normal((n, hk, d))
+        logical.append((k, v))
+        for p in range(npg[b]):
+            maps[b, p] = order[nxt]
+            nxt += 1
+        for t in range(n):
+            ck[maps[b, t // P], :, t % P] = k[t]
+            cv[maps[b, t // P], :, t % P] = v[t]
+    if v_layout == O.TRANSPOSED:
+        cv = np.ascontiguousarray(cv.transpose(1, 3, 0, 2).reshape(hk, d, n_phys * P))
+    return ck, cv, maps, logical
+
+
+@pytest.mark.parametrize("v_layout", [O.ROWMAJOR, O.TRANSPOSED])
+def test_decode_matches_torch_sdpa_per_sequence(v_layout):
+    """Each sequence's step equals torch SDPA (fp64, no mask) over its own logical keys, whatever
+    page the keys sit on; NaN in every slot the query must not see changes nothing."""
+    rng = np.random.default_rng(31)
+    lens, hk, g, d = (1, 15, 16, 17, 40, 0), 2, 3, 16
+    ck, cv, maps, logical = _paged_values(rng, lens, hk, d, v_layout)
+    q = rng.standard_normal((len(lens), hk * g, d))
+    got = O.decode_attention(q, ck, cv, maps, lens, 16, v_layout)
+    for b, n in enumerate(lens):
+        if n == 0:
+            assert np.array_equal(got[b], np.zeros_like(got[b]))
+            continue
+        k, v = logical[b]
+        qt = torch.tensor(q[b])[:, None, :]                                   # [Hq][1][D]
+        kt = torch.tensor(k).permute(1, 0, 2).repeat_interleave(g, 0)         # [Hq][n][D]
+        vt = torch.tensor(v).permute(1, 0, 2).repeat_interleave(g, 0)
+        ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt)[:, 0, :].numpy()
+        assert np.max(np.abs(got[b] - ref)) < 1e-12, b
+
+
+def test_decode_single_key_and_constant_values():
+    """Closed forms: with one cached token the output is that token's value row; when every value
+    row of a KV head is the same vector c, the output is c whatever the scores."""
+    rng = np.random.default_rng(32)
+    hk, g, d = 2, 2, 8
+    ck, cv, maps, logical = _paged_values(rng, (1, 37), hk, d, O.ROWMAJOR)
+    q = rng.standard_normal((2, hk * g, d))
+    got = O.decode_attention(q, ck, cv, maps, (1, 37), 16)
+    v0 = logical[0][1][0]                                                      # [hk][d]
+    assert np.allclose(got[0], np.repeat(v0, g, axis=0), atol=1e-15)
+    c = rng.standard_normal((hk, d))
+    cv2 = np.where(np.isnan(cv), np.nan, 0.0) + c[None, :, None, :]
+    got2 = O.decode_attention(q, ck, cv2, maps, (1, 37), 16, softcap=5.0)
+    assert np.allclose(got2[1], np.repeat(c, g, axis=0), atol=1e-13)
+
+
+def test_decode_shared_pages_and_softcap_limit():
+    """Two sequences whose tokens are equal give equal outputs whether they share physical pages
+    or not; a soft-cap far above every score changes the output by less than its O(s^3/cap^2)
+    bound, and a small cap flattens the distribution toward the mean value row."""
+    rng = np.random.default_rng(33)
+    hk, g, d, P = 1, 4, 16, 16
+    n = 50
+    k = rng.standard_normal((n, hk, d))
+    v = rng.standard_normal((n, hk, d))
+    ck = np.full((9, hk, P, d), np.nan)
+    cv = np.full((9, hk, P, d), np.nan)
+    maps = np.array([[0, 1, 2, 3], [0, 1, 5, 6]])                               # shared 32-token prefix
+    for t in range(n):
+        for b in range(2):
+            ck[maps[b, t // P], :, t % P] = k[t]
+            cv[maps[b, t // P], :, t % P] = v[t]
+    q1 = rng.standard_normal((1, hk * g, d))
+    q = np.concatenate([q1, q1])
+    got = O.decode_attention(q, ck, cv, maps, (n, n), P)
+    assert np.array_equal(got[0], got[1])
+    big = O.decode_attention(q, ck, cv, maps, (n, n), P, softcap=1e6)
+    assert np.max(np.abs(big - got)) < 1e-9
+    flat = O.decode_attention(q, ck, cv, maps, (n, n), P, softcap=1e-9)
+    assert np.allclose(flat[0], np.repeat(v.mean(axis=0), g, axis=0), atol=1e-6)
