@@ -254,6 +254,47 @@ size_t nexus_decode_attn_workspace(int32_t n_seqs, int32_t n_q_heads, const nexu
                                    int32_t max_seq_len);
 
 /*
+ * Warm-prefix reuse on the paged cache (the exact-token prefix arena of Sec. VI-D, whose copy
+ * within a pre-reserved arena becomes page-table work here).  Both calls take two DEVICE int32
+ * page maps of one cache (n_map_pages entries each, logical page -> physical page) and move
+ * every layer and KV head.  Entries of the pages a call touches must be in [0, n_phys_pages);
+ * they are not checked.
+ *
+ * nexus_kv_copy_tokens: logical tokens [t0, t0 + n_tokens) of the destination receive the K
+ * and V bits of the same logical tokens of the source; nothing else is written.  A logical page
+ * that both maps send to the same physical page is skipped (it is already shared).  Checks:
+ * n_tokens > 0 (NEXUS_EINVAL); 0 <= t0, t0 + n_tokens <= 16 * n_map_pages (NEXUS_ERANGE).
+ *
+ * nexus_kv_share_prefix: the first n_tokens tokens of the source become those of the
+ * destination.  Whole pages are shared by reference: dst_map[p] = src_map[p] for
+ * p < n_tokens / 16, written on the device.  The partial last page, if any, keeps the
+ * destination's own physical page (dst_map[n_tokens / 16], which must differ from the
+ * source's so that the destination can append after the prefix) and receives a copy of its
+ * n_tokens % 16 slots.  One kernel launch; nothing is enqueued when n_tokens == 0.  The caller
+ * owns page lifetimes (a shared page must outlive every map that names it).  Checks:
+ * 0 <= n_tokens <= 16 * n_map_pages (NEXUS_ERANGE).
+ */
+nexus_status nexus_kv_copy_tokens(const nexus_kv_cache *cache, const int32_t *src_map,
+                                  const int32_t *dst_map, int32_t n_map_pages, int64_t t0,
+                                  int32_t n_tokens, void *stream);
+nexus_status nexus_kv_share_prefix(const nexus_kv_cache *cache, const int32_t *src_map,
+                                   int32_t *dst_map, int32_t n_map_pages, int32_t n_tokens,
+                                   void *stream);
+
+/*
+ * Exact-token longest-common-prefix lookup over the slots of a warm-prefix arena (Sec. VI-D),
+ * host only.  slot_tokens is a HOST [n_slots][slot_stride] array whose slot s holds slot_len[s]
+ * tokens.  *slot receives the slot sharing the longest common prefix with tokens[0 .. n_tokens)
+ * (the lowest index among equals; -1 when no slot shares a first token) and *match_len its
+ * length.  Checks: non-negative sizes and non-NULL arrays where sizes are positive
+ * (NEXUS_EINVAL); 0 <= slot_len[s] <= slot_stride (NEXUS_ERANGE).
+ */
+nexus_status nexus_l0_longest_prefix(const int32_t *tokens, int32_t n_tokens,
+                                     const int32_t *slot_tokens, const int32_t *slot_len,
+                                     int32_t n_slots, int32_t slot_stride, int32_t *slot,
+                                     int32_t *match_len);
+
+/*
  * Redecode length of eq. (adaptive): ceil(S * R(n_past) / 100) with R = r_base for n_past <= M
  * and R = r_base + (n_past - M) / (M (K - 1)) * (100 - r_base) above, clamped to 100 (Sec. III-C;
  * the suffix length of Sec. VI-A).  Exact integer arithmetic.  Host only; returns -1 unless

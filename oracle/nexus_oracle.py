@@ -17,6 +17,8 @@ What it computes (paper sections cited per function):
   re-decoded suffix, with optional Gemma-2-style tanh logit soft-capping (Sec. VI-B names the
   soft-capped model family).  Full rows, two-pass softmax.
 * The decode step that follows: one query per sequence over that sequence's own page map.
+* Warm-prefix reuse (Sec. VI-D): exact-token longest-common-prefix match over arena slots, and
+  copying or sharing a prefix's K/V between two page maps.
 * The depth-adaptive recompute fraction R(n_past) of eq. (adaptive) and the redecode length
   ceil(S * R / 100) of Sec. VI-A, in exact rational arithmetic.
 * Round-to-nearest-even from fp64 to bfloat16, used to round re-phased keys back to the
@@ -325,6 +327,52 @@ def decode_attention(q: np.ndarray, cache_k: np.ndarray, cache_v: np.ndarray,
         k, v = gather_logical(cache_k[None], cache_v[None], page_maps[b], n, page_size, v_layout)
         out[b] = suffix_attention(q[b:b + 1], k[0], v[0], n - 1, scale, softcap)[0]
     return out
+
+
+# --------------------------------------------------------------------------------------
+# Warm-prefix reuse (Sec. VI-D): exact-token prefix match and KV copy / share on pages
+# --------------------------------------------------------------------------------------
+def longest_prefix(tokens, slots):
+    """(slot, length): the slot whose token list shares the longest common prefix with
+    ``tokens``, lowest index among equals; (-1, 0) when none shares a first token."""
+    best, best_len = -1, 0
+    for s, toks in enumerate(slots):
+        n = 0
+        while n < min(len(toks), len(tokens)) and toks[n] == tokens[n]:
+            n += 1
+        if n > best_len:
+            best, best_len = s, n
+    return best, best_len
+
+
+def copy_tokens(cache_k: np.ndarray, cache_v: np.ndarray, src_map, dst_map, t0: int,
+                n_tokens: int, page_size: int, v_layout: str = ROWMAJOR):
+    """Every layer's K and V of logical tokens [t0, t0 + n_tokens) under ``dst_map`` become
+    those under ``src_map``; all other bits are kept.  Raw-bit caches as ``splice_paged``."""
+    ck = np.array(cache_k, copy=True)
+    cv = np.array(cache_v, copy=True)
+    for t in range(t0, t0 + n_tokens):
+        ps, pd = int(src_map[t // page_size]), int(dst_map[t // page_size])
+        slot = t % page_size
+        ck[:, pd, :, slot, :] = cache_k[:, ps, :, slot, :]
+        if v_layout == ROWMAJOR:
+            cv[:, pd, :, slot, :] = cache_v[:, ps, :, slot, :]
+        else:
+            cv[:, :, :, pd * page_size + slot] = cache_v[:, :, :, ps * page_size + slot]
+    return ck, cv
+
+
+def share_prefix(cache_k: np.ndarray, cache_v: np.ndarray, src_map, dst_map, n_tokens: int,
+                 page_size: int, v_layout: str = ROWMAJOR):
+    """The destination's first n_tokens tokens become the source's: its whole pages take the
+    source's physical pages, its partial last page (kept) receives a copy of the slots.
+    Returns (cache_k, cache_v, new dst_map)."""
+    n_full = n_tokens // page_size
+    new_map = np.array(dst_map, copy=True)
+    new_map[:n_full] = np.asarray(src_map)[:n_full]
+    ck, cv = copy_tokens(cache_k, cache_v, src_map, new_map, n_full * page_size,
+                         n_tokens - n_full * page_size, page_size, v_layout)
+    return ck, cv, new_map
 
 
 # --------------------------------------------------------------------------------------

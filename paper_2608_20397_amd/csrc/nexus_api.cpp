@@ -506,4 +506,85 @@ nexus_status nexus_decode_attn(const void *q, int32_t n_seqs, int32_t n_q_heads,
 }
 
 
+namespace {
+
+nexus_status prepare_kv_copy(const nexus_kv_cache *cache, const int32_t *src_map,
+                             const int32_t *dst_map, int32_t n_map_pages, KvCopyLaunch &L) {
+  nexus_status st = check_cache(cache);
+  if (st) return st;
+  if (!src_map || !dst_map || n_map_pages <= 0) return NEXUS_EINVAL;
+  L = KvCopyLaunch{};
+  L.cache_k = cache->k;
+  L.cache_v = cache->v;
+  L.src_map = src_map;
+  L.dst_map = dst_map;
+  L.n_layers = cache->n_layers;
+  L.n_phys_pages = cache->n_phys_pages;
+  L.n_kv_heads = cache->n_kv_heads;
+  L.head_dim = cache->head_dim;
+  L.dtype_bytes = dtype_bytes(cache->dtype);
+  L.v_transposed = cache->v_layout == NEXUS_V_TRANSPOSED;
+  return NEXUS_OK;
+}
+
+}  // namespace
+
+nexus_status nexus_kv_copy_tokens(const nexus_kv_cache *cache, const int32_t *src_map,
+                                  const int32_t *dst_map, int32_t n_map_pages, int64_t t0,
+                                  int32_t n_tokens, void *stream) {
+  KvCopyLaunch L;
+  nexus_status st = prepare_kv_copy(cache, src_map, dst_map, n_map_pages, L);
+  if (st) return st;
+  if (n_tokens <= 0) return NEXUS_EINVAL;
+  if (t0 < 0 || t0 + n_tokens > (int64_t)n_map_pages * kPageSize) return NEXUS_ERANGE;
+  L.t0 = t0;
+  L.n_tokens = n_tokens;
+  return from_hip(launch_kv_copy(L, as_stream(stream)));
+}
+
+nexus_status nexus_kv_share_prefix(const nexus_kv_cache *cache, const int32_t *src_map,
+                                   int32_t *dst_map, int32_t n_map_pages, int32_t n_tokens,
+                                   void *stream) {
+  KvCopyLaunch L;
+  nexus_status st = prepare_kv_copy(cache, src_map, dst_map, n_map_pages, L);
+  if (st) return st;
+  if (n_tokens < 0 || n_tokens > (int64_t)n_map_pages * kPageSize) return NEXUS_ERANGE;
+  if (n_tokens == 0) return NEXUS_OK;
+  const int32_t n_full = n_tokens / kPageSize;
+  L.share_map = dst_map;
+  L.share_n_full = n_full;
+  L.t0 = (int64_t)n_full * kPageSize;
+  L.n_tokens = n_tokens - n_full * kPageSize;
+  return from_hip(launch_kv_copy(L, as_stream(stream)));
+}
+
+nexus_status nexus_l0_longest_prefix(const int32_t *tokens, int32_t n_tokens,
+                                     const int32_t *slot_tokens, const int32_t *slot_len,
+                                     int32_t n_slots, int32_t slot_stride, int32_t *slot,
+                                     int32_t *match_len) {
+  if (!slot || !match_len) return NEXUS_EINVAL;
+  *slot = -1;
+  *match_len = 0;
+  if (n_tokens < 0 || n_slots < 0 || slot_stride < 0) return NEXUS_EINVAL;
+  if ((n_tokens > 0 && !tokens) || (n_slots > 0 && (!slot_tokens || !slot_len)))
+    return NEXUS_EINVAL;
+  for (int32_t s = 0; s < n_slots; ++s)
+    if (slot_len[s] < 0 || slot_len[s] > slot_stride) return NEXUS_ERANGE;
+  int32_t best = 0;
+  for (int32_t s = 0; s < n_slots; ++s) {
+    const int32_t *st = slot_tokens + (size_t)s * slot_stride;
+    const int32_t lim = slot_len[s] < n_tokens ? slot_len[s] : n_tokens;
+    if (lim <= best) continue;          // cannot beat the current match
+    int32_t m = 0;
+    while (m < lim && st[m] == tokens[m]) ++m;
+    if (m > best) {
+      best = m;
+      *slot = s;
+    }
+  }
+  *match_len = best;
+  return NEXUS_OK;
+}
+
+
 }  // extern "C"

@@ -83,6 +83,11 @@ def lib():
         "nexus_decode_attn": (i32, [vp, i32, i32, pC, vp, i32, vp, i32, i32, f32, i32, f32, vp,
                                     vp, sz, vp]),
         "nexus_decode_attn_workspace": (sz, [i32, i32, pC, i32]),
+        "nexus_kv_copy_tokens": (i32, [pC, vp, vp, i32, i64, i32, vp]),
+        "nexus_kv_share_prefix": (i32, [pC, vp, vp, i32, i32, vp]),
+        "nexus_l0_longest_prefix": (i32, [C.POINTER(C.c_int32), i32, C.POINTER(C.c_int32),
+                                          C.POINTER(C.c_int32), i32, i32,
+                                          C.POINTER(C.c_int32), C.POINTER(C.c_int32)]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(L, name)
@@ -319,6 +324,55 @@ def decode_attn(q: torch.Tensor, cache: PagedKVCache, maps: torch.Tensor, seq_le
                                    _ptr(out), _ptr(ws), nbytes, _stream()),
            "nexus_decode_attn")
     return out
+
+
+def _map_arg(m: torch.Tensor, what: str):
+    if m.dtype != torch.int32 or m.dim() != 1 or not m.is_contiguous() or not m.is_cuda:
+        raise NexusError(EINVAL, f"{what} must be a contiguous int32 device vector")
+    return _ptr(m)
+
+
+def kv_copy_tokens(cache: PagedKVCache, src_map: torch.Tensor, dst_map: torch.Tensor, t0: int,
+                   n_tokens: int):
+    """Copy logical tokens [t0, t0 + n_tokens) of every layer from the sequence mapped by
+    ``src_map`` to the sequence mapped by ``dst_map`` (device int32 maps of equal length)."""
+    if src_map.numel() != dst_map.numel():
+        raise NexusError(EINVAL, "maps differ in length")
+    cc = cache.c()
+    _check(lib().nexus_kv_copy_tokens(C.byref(cc), _map_arg(src_map, "src_map"),
+                                      _map_arg(dst_map, "dst_map"), src_map.numel(), t0,
+                                      n_tokens, _stream()), "nexus_kv_copy_tokens")
+
+
+def kv_share_prefix(cache: PagedKVCache, src_map: torch.Tensor, dst_map: torch.Tensor,
+                    n_tokens: int):
+    """Share the first n_tokens tokens of the source with the destination: whole pages by
+    reference (dst_map is updated on the device), the partial last page by copy."""
+    if src_map.numel() != dst_map.numel():
+        raise NexusError(EINVAL, "maps differ in length")
+    cc = cache.c()
+    _check(lib().nexus_kv_share_prefix(C.byref(cc), _map_arg(src_map, "src_map"),
+                                       _map_arg(dst_map, "dst_map"), src_map.numel(), n_tokens,
+                                       _stream()), "nexus_kv_share_prefix")
+
+
+def l0_longest_prefix(tokens, slots):
+    """(slot, length) of the slot sharing the longest common prefix with ``tokens`` (host)."""
+    import numpy as np
+    t = np.ascontiguousarray(np.asarray(tokens, dtype=np.int32))
+    n_slots = len(slots)
+    stride = max([len(x) for x in slots] + [1])
+    arr = np.zeros((max(n_slots, 1), stride), dtype=np.int32)
+    lens = np.zeros(max(n_slots, 1), dtype=np.int32)
+    for i, x in enumerate(slots):
+        arr[i, :len(x)] = x
+        lens[i] = len(x)
+    P = C.POINTER(C.c_int32)
+    slot, mlen = C.c_int32(0), C.c_int32(0)
+    _check(lib().nexus_l0_longest_prefix(t.ctypes.data_as(P), t.size, arr.ctypes.data_as(P),
+                                         lens.ctypes.data_as(P), n_slots, stride, C.byref(slot),
+                                         C.byref(mlen)), "nexus_l0_longest_prefix")
+    return slot.value, mlen.value
 
 
 def redecode_len(S: int, n_past: int, M: int = 256, r_base_pct: int = 5, K: int = 4) -> int:

@@ -268,3 +268,54 @@ def test_status_strings():
     for st in range(9):
         assert len(L.nexus_status_str(st)) > 0
     assert L.nexus_status_str(99) == b"unknown status"
+
+
+def test_l0_longest_prefix_matches_oracle():
+    """Host logic of the warm-prefix arena lookup against the oracle's definition (32 slots)."""
+    import oracle as O
+    rng = np.random.default_rng(5)
+    for trial in range(200):
+        base = list(rng.integers(0, 3, size=int(rng.integers(0, 40))))
+        slots = []
+        for s in range(int(rng.integers(0, 33))):
+            k = int(rng.integers(0, len(base) + 1))
+            tail = list(rng.integers(0, 3, size=int(rng.integers(0, 10))))
+            slots.append(base[:k] + tail)
+        q = base[:int(rng.integers(0, len(base) + 1))] + list(rng.integers(0, 3, size=3))
+        assert N.l0_longest_prefix(q, slots) == O.longest_prefix(q, slots), trial
+    assert N.l0_longest_prefix([], [[1, 2]]) == (-1, 0)
+    assert N.l0_longest_prefix([1, 2], []) == (-1, 0)
+
+
+def test_kv_copy_and_share_validation_fails_closed():
+    L = N.lib()
+    buf, cache, block, pt = _setup(D=64)
+    s = C.c_void_p(0)
+    a, b = buf(8 * 4), buf(8 * 4)
+    f = L.nexus_kv_copy_tokens
+    assert f(None, a, b, 8, 0, 5, s) == N.EINVAL
+    assert f(C.byref(cache), None, b, 8, 0, 5, s) == N.EINVAL
+    assert f(C.byref(cache), a, None, 8, 0, 5, s) == N.EINVAL
+    assert f(C.byref(cache), a, b, 0, 0, 5, s) == N.EINVAL
+    assert f(C.byref(cache), a, b, 8, 0, 0, s) == N.EINVAL
+    assert f(C.byref(cache), a, b, 8, -1, 5, s) == N.ERANGE
+    assert f(C.byref(cache), a, b, 8, 120, 9, s) == N.ERANGE          # 129 > 128
+    g = L.nexus_kv_share_prefix
+    assert g(C.byref(cache), a, b, 8, -1, s) == N.ERANGE
+    assert g(C.byref(cache), a, b, 8, 129, s) == N.ERANGE
+    assert g(C.byref(cache), a, b, 8, 0, s) == N.OK                   # nothing to do
+    bc = N.CKvCache.from_buffer_copy(cache); bc.page_size = 32
+    assert g(C.byref(bc), a, b, 8, 5, s) == N.ESHAPE
+    P = C.POINTER(C.c_int32)
+    t = (C.c_int32 * 3)(1, 2, 3)
+    sl = (C.c_int32 * 2)(1, 2)
+    ln = (C.c_int32 * 1)(2)
+    out_s, out_l = C.c_int32(7), C.c_int32(7)
+    h = L.nexus_l0_longest_prefix
+    assert h(t, 3, sl, ln, 1, 2, None, C.byref(out_l)) == N.EINVAL
+    assert h(t, -1, sl, ln, 1, 2, C.byref(out_s), C.byref(out_l)) == N.EINVAL
+    assert h(None, 3, sl, ln, 1, 2, C.byref(out_s), C.byref(out_l)) == N.EINVAL
+    bad = (C.c_int32 * 1)(3)
+    assert h(t, 3, sl, bad, 1, 2, C.byref(out_s), C.byref(out_l)) == N.ERANGE
+    assert h(t, 3, sl, ln, 1, 2, C.byref(out_s), C.byref(out_l)) == N.OK
+    assert (out_s.value, out_l.value) == (0, 2)

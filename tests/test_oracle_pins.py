@@ -486,3 +486,52 @@ def test_decode_shared_pages_and_softcap_limit():
     assert np.max(np.abs(big - got)) < 1e-9
     flat = O.decode_attention(q, ck, cv, maps, (n, n), P, softcap=1e-9)
     assert np.allclose(flat[0], np.repeat(v.mean(axis=0), g, axis=0), atol=1e-6)
+
+
+# ---------------------------------------------------------------- warm-prefix reuse (Sec. VI-D)
+@settings(max_examples=60, deadline=None)
+@given(st.lists(st.lists(st.integers(0, 3), max_size=12), max_size=6),
+       st.lists(st.integers(0, 3), max_size=12))
+def test_longest_prefix_matches_commonprefix(slots, tokens):
+    """Library routine: os.path.commonprefix over lists gives each slot's common prefix."""
+    got = O.longest_prefix(tokens, slots)
+    lens = [len(os.path.commonprefix([s, tokens])) for s in slots]
+    best = max(lens, default=0)
+    if best == 0:
+        assert got == (-1, 0)
+    else:
+        assert got == (lens.index(best), best)
+
+
+@pytest.mark.parametrize("v_layout", [O.ROWMAJOR, O.TRANSPOSED])
+def test_copy_and_share_move_exactly_the_range(v_layout):
+    """Copy: the destination's logical range reads back as the source's, every other bit
+    unchanged, and a page both maps share is left alone.  Share: whole pages are aliased, the
+    partial page is the destination's own and holds the source's slots, its later slots keep
+    their bits."""
+    rng = np.random.default_rng(41)
+    L, npg, H, P, D = 2, 12, 2, 16, 8
+    ck = rng.integers(0, 1 << 16, (L, npg, H, P, D), dtype=np.uint16)
+    cv = (rng.integers(0, 1 << 16, (L, H, D, npg * P), dtype=np.uint16) if v_layout == O.TRANSPOSED
+          else rng.integers(0, 1 << 16, (L, npg, H, P, D), dtype=np.uint16))
+    src = np.array([3, 7, 1, 9, 4])
+    dst = np.array([3, 2, 8, 0, 11])                         # logical page 0 is shared
+    t0, n = 5, 60
+    nk, nv = O.copy_tokens(ck, cv, src, dst, t0, n, P, v_layout)
+    sk, sv = O.gather_logical(ck, cv, src, 5 * P, P, v_layout)
+    dk, dv = O.gather_logical(nk, nv, dst, 5 * P, P, v_layout)
+    assert np.array_equal(dk[:, t0:t0 + n], sk[:, t0:t0 + n])
+    assert np.array_equal(dv[:, t0:t0 + n], sv[:, t0:t0 + n])
+    ok, ov = O.gather_logical(ck, cv, dst, 5 * P, P, v_layout)
+    for a, b in ((dk, ok), (dv, ov)):
+        assert np.array_equal(a[:, t0 + n:], b[:, t0 + n:])
+        assert np.array_equal(a[:, P:t0], b[:, P:t0]) if t0 > P else True
+    untouched = np.setdiff1d(np.arange(npg), dst[1:])
+    assert np.array_equal(nk[:, untouched], ck[:, untouched])
+    # share 37 tokens: pages 0, 1 aliased, page 2 (physical 8) gets slots 0..4
+    sk2, sv2, m2 = O.share_prefix(ck, cv, src, dst, 37, P, v_layout)
+    assert list(m2) == [3, 7, 8, 0, 11]
+    a_k, a_v = O.gather_logical(sk2, sv2, m2, 5 * P, P, v_layout)
+    assert np.array_equal(a_k[:, :37], sk[:, :37]) and np.array_equal(a_v[:, :37], sv[:, :37])
+    b_k, b_v = O.gather_logical(ck, cv, dst, 5 * P, P, v_layout)
+    assert np.array_equal(a_k[:, 37:48], b_k[:, 37:48]) and np.array_equal(a_v[:, 37:48], b_v[:, 37:48])
