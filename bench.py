@@ -269,6 +269,102 @@ def time_next_rows(S, reps: int):
     return out
 
 
+def _graph_time(fn, reps: int, inner: int = 1):
+    """Mean ms of ``fn``'s launches, captured ``inner`` times in one HIP graph and replayed (no
+    host overhead; a graph launch's own cost is spread over ``inner`` calls)."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(st):
+        with torch.cuda.graph(g, stream=st):
+            for _ in range(inner):
+                fn()
+    torch.cuda.current_stream().wait_stream(st)
+    g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / (reps * inner)
+
+
+def time_decode(S, reps: int):
+    """Decode step and warm-prefix reuse after the measured steps.
+
+    * decode_b1: one query over the whole spliced cache of the step (all cache tokens, its own
+      page map), every layer, captured in a HIP graph;
+    * decode_b32: 32 sequences of the same depth on private pages (8 layers of synthetic K/V),
+      the warm-prefix pool's width;
+    * share_prefix: the first 16384 + 5 tokens of one of those sequences shared with another
+      (1024 pages by reference, 5 slots of each of the 8 layers copied), one launch;
+    * copy_tokens: a 16384-token prefix copied into a third sequence's pages (the copy the
+      paper's arena performs), 8 layers.
+    GB/s on algorithmic bytes: K and V of every attended key plus q and out (decode); read +
+    write of the copied slots (share, copy)."""
+    import torch
+    from paper_2608_20397_amd import nexus as N
+    wl, cache = S["wl"], S["cache"]
+    L, H, D, Hq = wl.n_layers, wl.n_kv_heads, wl.head_dim, wl.n_q_heads
+    es = 2 if wl.dtype == "bf16" else 4
+    dev = cache.k.device
+    n = wl.n_tokens
+    out = {}
+
+    def decode_case(cch, n_seqs, layers, maps, tag):
+        lens = torch.full((n_seqs,), n, dtype=torch.int32, device=dev)
+        q = torch.randn((layers, n_seqs, Hq, D), device=dev).to(cache.k.dtype)
+        o = torch.empty_like(q[0])
+        wsb = N.decode_attn_workspace_bytes(cch, n_seqs, Hq, n)
+        ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+
+        def fn():
+            for l in range(layers):
+                N.decode_attn(q[l], cch, maps, lens, n, l, softcap=wl.softcap, out=o, workspace=ws)
+        ms = _graph_time(fn, max(reps, 3)) / layers
+        nbytes = n_seqs * (2 * n * H * D * es + 2 * Hq * D * es)
+        out[tag] = {"sequences": n_seqs, "tokens_each": n, "layers_timed": layers,
+                    "mean_launch_ms": ms, "bytes_per_launch": nbytes,
+                    "achieved_GBps": nbytes / (ms * 1e-3) / 1e9,
+                    "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+
+    n_pages = -(-n // 16)
+    decode_case(cache, 1, L, cache.page_map[:n_pages].reshape(1, n_pages).contiguous(),
+                "decode_b1")
+    B, L8 = 32, 8
+    npp = B * n_pages
+    k = torch.randn((L8, npp, H, 16, D), device=dev).to(cache.k.dtype)
+    v = torch.randn((L8, npp, H, 16, D), device=dev).to(cache.k.dtype)
+    c32 = N.PagedKVCache(k, v, torch.zeros(1, dtype=torch.int32, device=dev), wl.rope_base,
+                         N.V_ROWMAJOR)
+    maps = torch.arange(npp, dtype=torch.int32, device=dev).view(B, n_pages).contiguous()
+    decode_case(c32, B, L8, maps, "decode_b32")
+    # warm-prefix reuse between two sequences of the 32-sequence cache (disjoint pages)
+    src, dst = maps[0].contiguous(), maps[1].contiguous()
+    slot_bytes = 2 * L8 * H * D * es                      # K and V of one token, all layers
+    n_share = 16384 + 5
+    # idempotent after its first run: 50 calls per graph
+    ms = _graph_time(lambda: N.kv_share_prefix(c32, src, dst, n_share), max(reps, 3), inner=50)
+    tail = n_share % 16
+    out["share_prefix"] = {"tokens": n_share, "layers": L8, "pages_shared": n_share // 16,
+                           "slots_copied": tail, "mean_launch_ms": ms,
+                           "bytes_per_launch": 2 * tail * slot_bytes}
+    n_copy = 16384
+    dst2 = maps[2].contiguous()
+    ms = _graph_time(lambda: N.kv_copy_tokens(c32, src, dst2, 0, n_copy), max(reps, 3))
+    nbytes = 2 * n_copy * slot_bytes
+    out["copy_tokens"] = {"tokens": n_copy, "layers": L8, "mean_launch_ms": ms,
+                          "bytes_per_launch": nbytes, "achieved_GBps": nbytes / (ms * 1e-3) / 1e9,
+                          "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+    del k, v, c32, maps
+    return out
+
+
 SWEEP_DEPTHS = (256, 512, 1024, 2048, 4096, 16384)
 
 
@@ -492,6 +588,7 @@ def main():
         },
     }
     res["next_rows"] = time_next_rows(S, args.steps)
+    res["next_rows"].update(time_decode(S, args.steps))
     try:
         res["git"] = subprocess.run(["git", "-C", ROOT, "rev-parse", "--short", "HEAD"],
                                     capture_output=True, text=True).stdout.strip() or None

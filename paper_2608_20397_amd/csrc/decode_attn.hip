@@ -27,7 +27,7 @@
 // Key rows past the sequence end are never used: the last page's loads re-read the last valid
 // row (row-major) or are zeroed (transposed V), and their scores are -inf.
 #include "attn_common.h"
-#include "launch.h"
+#include "launch_decode.h"
 
 namespace nexus {
 

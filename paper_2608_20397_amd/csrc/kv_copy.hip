@@ -8,7 +8,7 @@
 // transposed V holds each (head, feature) row token-innermost: the run is (s1 - s0) elements
 // per row, copied as 16-byte chunks when the page is whole and element by element otherwise.
 #include "device_common.h"
-#include "launch.h"
+#include "launch_decode.h"
 
 namespace nexus {
 

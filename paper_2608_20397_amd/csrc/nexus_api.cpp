@@ -10,6 +10,7 @@
 #include <vector>
 
 #include "launch.h"
+#include "launch_decode.h"
 
 using namespace nexus;
 
