@@ -295,6 +295,40 @@ nexus_status nexus_l0_longest_prefix(const int32_t *tokens, int32_t n_tokens,
                                      int32_t *match_len);
 
 /*
+ * Semantic Lookaside Buffer (Sec. V-A): tool embeddings INT8-quantised and scanned with integer
+ * dot products; the top-two margin gate decides between auto-routing and escalation.
+ *
+ * nexus_slb_quantize: symmetric per-row INT8 codes of x [n][dim] (fp32, device):
+ * scale[r] = max_j |x[r][j]| / 127 and q[r][j] = x[r][j] / scale[r] rounded to nearest-even
+ * (IEEE fp32 division), so |q| <= 127; a row of zeros gets scale 0 and zero codes.  For the
+ * registry (offline) and for each query embedding.  Checks: non-NULL, n > 0, dim > 0
+ * (NEXUS_EINVAL).
+ *
+ * nexus_slb_scan: for every query q of queries [n_queries][dim] (int8, device, rows 16-byte
+ * aligned) against tools [n_tools][dim] (int8, device), the score of tool t is
+ * (float(dot(tools[t], queries[q])) * tool_scale[t]) * query_scale[q] in fp32, each product
+ * rounded to nearest-even (the integer dot is exact).  Outputs per query, device arrays:
+ *   top_idx [n_queries][k], top_score [n_queries][k]: the k best tools, higher score first and
+ *     the lower index first among equal scores; index -1 and score -inf past n_tools;
+ *   margin [n_queries]: top_score[0] - top_score[1] in fp32 (+inf when n_tools == 1);
+ *   route [n_queries]: 1 when margin > tau (auto-route), else 0 (escalate to the reranker).
+ *   The paper calibrates tau = 0.0136 (the 20th percentile of adversarial-pair margins).
+ * workspace: nexus_slb_scan_workspace() bytes (NULL allowed when 0).  Checks: non-NULL arrays,
+ * n_tools > 0, n_queries > 0, 1 <= k <= 8, finite tau (NEXUS_EINVAL); dim a multiple of 64 in
+ * [64, 1024] (NEXUS_ESHAPE).  Queries are processed in blocks of 64 on int8 MFMA, so a batch of
+ * queries costs little more than one.
+ */
+nexus_status nexus_slb_quantize(const float *x, int32_t n, int32_t dim, int8_t *q, float *scale,
+                                void *stream);
+nexus_status nexus_slb_scan(const int8_t *tools, const float *tool_scale, int32_t n_tools,
+                            const int8_t *queries, const float *query_scale, int32_t n_queries,
+                            int32_t dim, int32_t k, float tau, int32_t *top_idx,
+                            float *top_score, float *margin, int32_t *route, void *workspace,
+                            size_t workspace_bytes, void *stream);
+/* Workspace bytes nexus_slb_scan needs (0 if none, SIZE_MAX if the arguments are invalid). */
+size_t nexus_slb_scan_workspace(int32_t n_tools, int32_t n_queries, int32_t dim, int32_t k);
+
+/*
  * Redecode length of eq. (adaptive): ceil(S * R(n_past) / 100) with R = r_base for n_past <= M
  * and R = r_base + (n_past - M) / (M (K - 1)) * (100 - r_base) above, clamped to 100 (Sec. III-C;
  * the suffix length of Sec. VI-A).  Exact integer arithmetic.  Host only; returns -1 unless

@@ -17,6 +17,8 @@ What it computes (paper sections cited per function):
   re-decoded suffix, with optional Gemma-2-style tanh logit soft-capping (Sec. VI-B names the
   soft-capped model family).  Full rows, two-pass softmax.
 * The decode step that follows: one query per sequence over that sequence's own page map.
+* The Semantic Lookaside Buffer scan (Sec. V-A): INT8 quantisation, integer dot products, the
+  best tools per query and the top-two margin gate.
 * Warm-prefix reuse (Sec. VI-D): exact-token longest-common-prefix match over arena slots, and
   copying or sharing a prefix's K/V between two page maps.
 * The depth-adaptive recompute fraction R(n_past) of eq. (adaptive) and the redecode length
@@ -373,6 +375,52 @@ def share_prefix(cache_k: np.ndarray, cache_v: np.ndarray, src_map, dst_map, n_t
     ck, cv = copy_tokens(cache_k, cache_v, src_map, new_map, n_full * page_size,
                          n_tokens - n_full * page_size, page_size, v_layout)
     return ck, cv, new_map
+
+
+# --------------------------------------------------------------------------------------
+# Semantic Lookaside Buffer (Sec. V-A): INT8 scan and top-two margin gate
+# --------------------------------------------------------------------------------------
+def slb_quantize(x: np.ndarray):
+    """Symmetric per-row INT8 codes of fp32 rows: scale = max|x| / 127 and code =
+    rint(x / scale) (fp32 division, ties to even), within [-127, 127]; a zero row gets scale 0
+    and zero codes.  The INT8 tool and query vectors of Sec. V-A (its quantiser is not given;
+    this is the reading)."""
+    x = np.asarray(x, dtype=np.float32)
+    scale = (np.max(np.abs(x), axis=1) / np.float32(127)).astype(np.float32)
+    q = np.zeros(x.shape, dtype=np.int8)
+    for r in range(x.shape[0]):
+        if scale[r] > 0:
+            q[r] = np.clip(np.rint(x[r] / scale[r]), -127, 127).astype(np.int8)
+    return q, scale
+
+
+def slb_scan(tools_q: np.ndarray, tool_scale: np.ndarray, queries_q: np.ndarray,
+             query_scale: np.ndarray, k: int, tau: float):
+    """Scan every tool for every query and gate on the top-two margin (Sec. V-A).
+
+    Score = (float32(dot) * tool_scale) * query_scale, in fp32 with one rounding per product (the
+    integer dot is exact).  The k best tools per query, higher score first and the lower index
+    first among equal scores (index -1, score -inf past the registry); margin = s1 - s2 in fp32
+    (+inf with a single tool); route = margin > tau (auto-route) else escalate to the reranker.
+    Returns (top_idx [Q][k], top_score [Q][k], margin [Q], route [Q]).
+    """
+    dot = np.asarray(queries_q, dtype=np.int64) @ np.asarray(tools_q, dtype=np.int64).T
+    score = (dot.astype(np.float32) * np.asarray(tool_scale, np.float32)[None, :]) \
+        * np.asarray(query_scale, np.float32)[:, None]
+    n_q, n_t = score.shape
+    idx = np.full((n_q, k), -1, dtype=np.int32)
+    top = np.full((n_q, k), -np.inf, dtype=np.float32)
+    margin = np.zeros(n_q, dtype=np.float32)
+    route = np.zeros(n_q, dtype=np.int32)
+    for q in range(n_q):
+        order = sorted(range(n_t), key=lambda t: (-float(score[q, t]), t))
+        for j in range(min(k, n_t)):
+            idx[q, j] = order[j]
+            top[q, j] = score[q, order[j]]
+        margin[q] = np.float32(np.inf) if n_t < 2 else \
+            np.float32(score[q, order[0]] - score[q, order[1]])
+        route[q] = 1 if margin[q] > np.float32(tau) else 0
+    return idx, top, margin, route
 
 
 # --------------------------------------------------------------------------------------

@@ -11,6 +11,7 @@
 
 #include "launch.h"
 #include "launch_decode.h"
+#include "launch_slb.h"
 
 using namespace nexus;
 
@@ -585,6 +586,65 @@ nexus_status nexus_l0_longest_prefix(const int32_t *tokens, int32_t n_tokens,
   }
   *match_len = best;
   return NEXUS_OK;
+}
+
+
+nexus_status nexus_slb_quantize(const float *x, int32_t n, int32_t dim, int8_t *q, float *scale,
+                                void *stream) {
+  if (!x || !q || !scale || n <= 0 || dim <= 0) return NEXUS_EINVAL;
+  if ((int64_t)n * dim >= kMaxElems32 * 2) return NEXUS_ESHAPE;
+  return from_hip(launch_slb_quantize(x, n, dim, q, scale, as_stream(stream)));
+}
+
+namespace {
+
+nexus_status check_slb(const void *tools, const float *tool_scale, int32_t n_tools,
+                       const void *queries, const float *query_scale, int32_t n_queries,
+                       int32_t dim, int32_t k, float tau) {
+  if (!tools || !tool_scale || !queries || !query_scale) return NEXUS_EINVAL;
+  if (n_tools <= 0 || n_queries <= 0 || k < 1 || k > 8) return NEXUS_EINVAL;
+  if (!isfinite(tau)) return NEXUS_EINVAL;
+  if (dim <= 0 || dim % 64 || dim > 1024) return NEXUS_ESHAPE;
+  if ((int64_t)n_tools * dim >= ((int64_t)1 << 40)) return NEXUS_ESHAPE;
+  if (n_queries > 65535 * 64) return NEXUS_ESHAPE;
+  return NEXUS_OK;
+}
+
+}  // namespace
+
+size_t nexus_slb_scan_workspace(int32_t n_tools, int32_t n_queries, int32_t dim, int32_t k) {
+  if (n_tools <= 0 || n_queries <= 0 || k < 1 || k > 8 || dim <= 0 || dim % 64 || dim > 1024)
+    return SIZE_MAX;
+  return slb_workspace_bytes(n_tools, n_queries, dim);
+}
+
+nexus_status nexus_slb_scan(const int8_t *tools, const float *tool_scale, int32_t n_tools,
+                            const int8_t *queries, const float *query_scale, int32_t n_queries,
+                            int32_t dim, int32_t k, float tau, int32_t *top_idx,
+                            float *top_score, float *margin, int32_t *route, void *workspace,
+                            size_t workspace_bytes, void *stream) {
+  nexus_status st = check_slb(tools, tool_scale, n_tools, queries, query_scale, n_queries, dim,
+                              k, tau);
+  if (st) return st;
+  if (!top_idx || !top_score || !margin || !route) return NEXUS_EINVAL;
+  const size_t need = slb_workspace_bytes(n_tools, n_queries, dim);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return NEXUS_EWORKSPACE;
+  SlbLaunch L{};
+  L.tools = tools;
+  L.tool_scale = tool_scale;
+  L.queries = queries;
+  L.query_scale = query_scale;
+  L.n_tools = n_tools;
+  L.n_queries = n_queries;
+  L.dim = dim;
+  L.k = k;
+  L.tau = tau;
+  L.top_idx = top_idx;
+  L.top_score = top_score;
+  L.margin = margin;
+  L.route = route;
+  L.workspace = workspace;
+  return from_hip(launch_slb_scan(L, as_stream(stream)));
 }
 
 

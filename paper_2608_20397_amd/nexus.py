@@ -88,6 +88,10 @@ def lib():
         "nexus_l0_longest_prefix": (i32, [C.POINTER(C.c_int32), i32, C.POINTER(C.c_int32),
                                           C.POINTER(C.c_int32), i32, i32,
                                           C.POINTER(C.c_int32), C.POINTER(C.c_int32)]),
+        "nexus_slb_quantize": (i32, [vp, i32, i32, vp, vp, vp]),
+        "nexus_slb_scan": (i32, [vp, vp, i32, vp, vp, i32, i32, i32, f32, vp, vp, vp, vp, vp, sz,
+                                 vp]),
+        "nexus_slb_scan_workspace": (sz, [i32, i32, i32, i32]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(L, name)
@@ -373,6 +377,50 @@ def l0_longest_prefix(tokens, slots):
                                          lens.ctypes.data_as(P), n_slots, stride, C.byref(slot),
                                          C.byref(mlen)), "nexus_l0_longest_prefix")
     return slot.value, mlen.value
+
+
+def slb_quantize(x: torch.Tensor):
+    """x [n][dim] fp32 (device) -> (int8 codes [n][dim], fp32 scales [n])."""
+    if x.dtype != torch.float32 or x.dim() != 2 or not x.is_contiguous() or not x.is_cuda:
+        raise NexusError(EINVAL, "x must be a contiguous fp32 [n][dim] device tensor")
+    n, dim = x.shape
+    q = torch.empty((n, dim), dtype=torch.int8, device=x.device)
+    s = torch.empty((n,), dtype=torch.float32, device=x.device)
+    _check(lib().nexus_slb_quantize(_ptr(x), n, dim, _ptr(q), _ptr(s), _stream()),
+           "nexus_slb_quantize")
+    return q, s
+
+
+def slb_scan(tools: torch.Tensor, tool_scale: torch.Tensor, queries: torch.Tensor,
+             query_scale: torch.Tensor, k: int = 2, tau: float = 0.0136,
+             workspace: torch.Tensor | None = None, out=None):
+    """Top-k tools per query, the top-two margin and the gate (1 = auto-route).  Returns
+    (top_idx [Q][k] int32, top_score [Q][k] fp32, margin [Q] fp32, route [Q] int32)."""
+    for t, dt, nd in ((tools, torch.int8, 2), (queries, torch.int8, 2),
+                      (tool_scale, torch.float32, 1), (query_scale, torch.float32, 1)):
+        if t.dtype != dt or t.dim() != nd or not t.is_contiguous() or not t.is_cuda:
+            raise NexusError(EINVAL, "slb_scan: bad operand dtype, shape or device")
+    n_tools, dim = tools.shape
+    n_q = queries.shape[0]
+    if queries.shape[1] != dim or tool_scale.numel() != n_tools or query_scale.numel() != n_q:
+        raise NexusError(ESHAPE, "slb_scan: operand shapes disagree")
+    dev = tools.device
+    if out is None:
+        out = (torch.empty((n_q, k), dtype=torch.int32, device=dev),
+               torch.empty((n_q, k), dtype=torch.float32, device=dev),
+               torch.empty((n_q,), dtype=torch.float32, device=dev),
+               torch.empty((n_q,), dtype=torch.int32, device=dev))
+    ws_bytes = lib().nexus_slb_scan_workspace(n_tools, n_q, dim, k)
+    if ws_bytes == (1 << 64) - 1:
+        ws_bytes = 0             # invalid arguments: the call itself reports which check failed
+    ws = _workspace(ws_bytes, dev, workspace)
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    idx, score, margin, route = out
+    _check(lib().nexus_slb_scan(_ptr(tools), _ptr(tool_scale), n_tools, _ptr(queries),
+                                _ptr(query_scale), n_q, dim, k, tau, _ptr(idx), _ptr(score),
+                                _ptr(margin), _ptr(route), _ptr(ws), nbytes, _stream()),
+           "nexus_slb_scan")
+    return out
 
 
 def redecode_len(S: int, n_past: int, M: int = 256, r_base_pct: int = 5, K: int = 4) -> int:

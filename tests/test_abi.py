@@ -319,3 +319,34 @@ def test_kv_copy_and_share_validation_fails_closed():
     assert h(t, 3, sl, bad, 1, 2, C.byref(out_s), C.byref(out_l)) == N.ERANGE
     assert h(t, 3, sl, ln, 1, 2, C.byref(out_s), C.byref(out_l)) == N.OK
     assert (out_s.value, out_l.value) == (0, 2)
+
+
+def test_slb_validation_fails_closed():
+    L = N.lib()
+    buf = _Bufs()
+    s = C.c_void_p(0)
+    t, ts, q, qs = buf(100 * 768), buf(400), buf(768), buf(4)
+    o1, o2, o3, o4 = buf(64), buf(64), buf(4), buf(4)
+    ok = dict(t=t, ts=ts, n=100, q=q, qs=qs, nq=1, dim=768, k=2, tau=0.0136)
+
+    def call(ws=None, wsb=0, **kw):
+        a = dict(ok, **kw)
+        return L.nexus_slb_scan(a["t"], a["ts"], a["n"], a["q"], a["qs"], a["nq"], a["dim"], a["k"],
+                                a["tau"], o1, o2, o3, o4, ws, wsb, s)
+
+    assert call(t=None) == N.EINVAL
+    assert call(qs=None) == N.EINVAL
+    assert call(n=0) == N.EINVAL
+    assert call(nq=0) == N.EINVAL
+    assert call(k=0) == N.EINVAL
+    assert call(k=9) == N.EINVAL
+    assert call(tau=float("nan")) == N.EINVAL
+    assert call(dim=100) == N.ESHAPE
+    assert call(dim=2048) == N.ESHAPE
+    need = L.nexus_slb_scan_workspace(100000, 256, 768, 8)
+    assert need > 0
+    assert call(n=100000, nq=256, k=8) == N.EWORKSPACE
+    assert L.nexus_slb_scan_workspace(100, 1, 100, 2) == (1 << 64) - 1
+    assert L.nexus_slb_scan_workspace(250, 1, 768, 2) == 0          # one range: no workspace
+    assert L.nexus_slb_quantize(None, 1, 64, o1, o2, s) == N.EINVAL
+    assert L.nexus_slb_quantize(t, 0, 64, o1, o2, s) == N.EINVAL

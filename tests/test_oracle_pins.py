@@ -535,3 +535,71 @@ def test_copy_and_share_move_exactly_the_range(v_layout):
     assert np.array_equal(a_k[:, :37], sk[:, :37]) and np.array_equal(a_v[:, :37], sv[:, :37])
     b_k, b_v = O.gather_logical(ck, cv, dst, 5 * P, P, v_layout)
     assert np.array_equal(a_k[:, 37:48], b_k[:, 37:48]) and np.array_equal(a_v[:, 37:48], b_v[:, 37:48])
+
+
+# ---------------------------------------------------------------- SLB scan and gate (Sec. V-A)
+def test_slb_quantize_bounds_and_extremes():
+    """Codes lie in [-127, 127]; each row's largest magnitude maps to +-127; dequantised values
+    are within half a step (plus fp32 rounding) of the input; a zero row stays zero."""
+    rng = np.random.default_rng(51)
+    x = rng.standard_normal((20, 96)).astype(np.float32) * rng.uniform(0.01, 10, (20, 1)).astype(np.float32)
+    x[3] = 0
+    q, s = O.slb_quantize(x)
+    assert q.dtype == np.int8 and np.abs(q.astype(int)).max() <= 127
+    for r in range(20):
+        if r == 3:
+            assert s[r] == 0 and not q[r].any()
+            continue
+        j = int(np.argmax(np.abs(x[r])))
+        assert abs(int(q[r, j])) == 127 and np.sign(q[r, j]) == np.sign(x[r, j])
+        err = np.abs(q[r].astype(np.float64) * s[r] - x[r])
+        assert err.max() <= 0.5 * s[r] * (1 + 1e-5) + 1e-7
+
+
+@settings(max_examples=40, deadline=None)
+@given(st.integers(1, 9), st.integers(1, 4), st.integers(1, 8), st.integers(0, 10**6))
+def test_slb_scan_matches_brute_force(n_tools, n_q, k, seed):
+    """Brute force on tiny inputs: every (query, tool) score from its definition, ranked by
+    (-score, index) with Python's sort; duplicate tools exercise the tie order."""
+    rng = np.random.default_rng(seed)
+    dim = 8
+    tq = rng.integers(-127, 128, (n_tools, dim)).astype(np.int8)
+    if n_tools > 2:
+        tq[2] = tq[0]                                       # a tie: tool 0 must rank first
+    ts = rng.uniform(0.001, 0.02, n_tools).astype(np.float32)
+    if n_tools > 2:
+        ts[2] = ts[0]
+    qq = rng.integers(-127, 128, (n_q, dim)).astype(np.int8)
+    qs = rng.uniform(0.001, 0.02, n_q).astype(np.float32)
+    tau = np.float32(rng.uniform(0, 0.05))
+    idx, top, margin, route = O.slb_scan(tq, ts, qq, qs, k, float(tau))
+    for q in range(n_q):
+        sc = []
+        for t in range(n_tools):
+            d = sum(int(qq[q, e]) * int(tq[t, e]) for e in range(dim))
+            sc.append(np.float32(np.float32(np.float32(d) * ts[t]) * qs[q]))
+        order = sorted(range(n_tools), key=lambda t: (-sc[t], t))
+        want = order[:k] + [-1] * (k - min(k, n_tools))
+        assert list(idx[q]) == want
+        if n_tools >= 2:
+            assert margin[q] == np.float32(sc[order[0]] - sc[order[1]])
+            assert route[q] == int(margin[q] > tau)
+        else:
+            assert np.isinf(margin[q]) and route[q] == 1
+
+
+def test_slb_scan_is_cosine_ranking_on_unit_vectors():
+    """On unit-norm vectors the INT8 score approximates the cosine similarity: the best tool is
+    the fp64 cosine argmax when that argmax leads by more than the quantisation error."""
+    rng = np.random.default_rng(52)
+    t = rng.standard_normal((300, 768))
+    t /= np.linalg.norm(t, axis=1, keepdims=True)
+    q = t[[5, 77, 123]] + 0.2 * rng.standard_normal((3, 768)) / np.sqrt(768)
+    q /= np.linalg.norm(q, axis=1, keepdims=True)
+    tq, ts = O.slb_quantize(t.astype(np.float32))
+    qq, qs = O.slb_quantize(q.astype(np.float32))
+    idx, top, margin, route = O.slb_scan(tq, ts, qq, qs, 2, 0.0136)
+    cos = q @ t.T
+    assert list(idx[:, 0]) == [5, 77, 123]
+    assert np.allclose(top[:, 0], cos[np.arange(3), [5, 77, 123]], atol=2e-3)
+    assert route.all()
