@@ -365,6 +365,68 @@ def time_decode(S, reps: int):
     return out
 
 
+def time_slb(reps: int):
+    """The SLB scan and margin gate (Sec. V-A) after the measured steps, each timed in a HIP
+    graph: the paper's registry (250 tools, one query, the query's quantisation included), a
+    1M-tool registry with one query (a pass over 768 MB of INT8 rows: GB/s against HBM) and a
+    serving batch (65536 tools x 256 queries: int8 TOPS)."""
+    import numpy as np
+    import torch
+    from paper_2608_20397_amd import nexus as N
+    from synth import slb as SL
+    dev = "cuda"
+    out = {}
+
+    def run(tq, ts, qq, qs, k, tag, extra=None, quantize=None):
+        n, dim = tq.shape
+        nq = qq.shape[0]
+        res = (torch.empty((nq, k), dtype=torch.int32, device=dev),
+               torch.empty((nq, k), device=dev), torch.empty(nq, device=dev),
+               torch.empty(nq, dtype=torch.int32, device=dev))
+        wsb = N.lib().nexus_slb_scan_workspace(n, nq, dim, k)
+        ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+
+        def fn():
+            if quantize is not None:
+                quantize()
+            N.slb_scan(tq, ts, qq, qs, k, 0.0136, workspace=ws, out=res)
+        inner = 20 if n * nq <= 1 << 22 else 3
+        ms = _graph_time(fn, max(reps, 3), inner=inner)
+        row = {"tools": n, "queries": nq, "dim": dim, "k": k, "mean_launch_ms": ms,
+               "tool_bytes": n * dim, "achieved_GBps": n * dim / (ms * 1e-3) / 1e9,
+               "int8_TOPS": 2.0 * n * nq * dim / (ms * 1e-3) / 1e12,
+               "route_rate": float(res[3].float().mean().item())}
+        row.update(extra or {})
+        out[tag] = row
+
+    # the paper's registry size, synthetic unit-norm vectors; the query quantised in the loop
+    t, q, _ = SL.slb_inputs(1)
+    tq, ts = N.slb_quantize(torch.from_numpy(t).to(dev))
+    qf = torch.from_numpy(q).to(dev)
+    qq = torch.empty((1, t.shape[1]), dtype=torch.int8, device=dev)
+    qs = torch.empty(1, device=dev)
+
+    def quant():
+        N.slb_quantize(qf, out=(qq, qs))
+    run(tq, ts, qq, qs, 3, "slb_n250_q1", {"includes": "query quantisation + scan + gate"},
+        quantize=quant)
+    g = torch.Generator(device=dev)
+    g.manual_seed(20397)
+    big = torch.randint(-127, 128, (1 << 20, 768), dtype=torch.int8, device=dev, generator=g)
+    bs = torch.rand(1 << 20, device=dev, generator=g) * 0.01
+    q1 = torch.randint(-127, 128, (1, 768), dtype=torch.int8, device=dev, generator=g)
+    s1 = torch.rand(1, device=dev, generator=g) * 0.01
+    run(big, bs, q1, s1, 8, "slb_n1m_q1")
+    out["slb_n1m_q1"]["frac_hbm"] = out["slb_n1m_q1"]["achieved_GBps"] / HBM_PEAK_GBPS
+    mid, ms_ = big[:65536], bs[:65536]
+    qb = torch.randint(-127, 128, (256, 768), dtype=torch.int8, device=dev, generator=g)
+    sb = torch.rand(256, device=dev, generator=g) * 0.01
+    run(mid, ms_, qb, sb, 8, "slb_n65536_q256")
+    out["slb_n65536_q256"]["frac_int8_mfma"] = out["slb_n65536_q256"]["int8_TOPS"] / 5000.0
+    del big
+    return out
+
+
 SWEEP_DEPTHS = (256, 512, 1024, 2048, 4096, 16384)
 
 
@@ -589,6 +651,7 @@ def main():
     }
     res["next_rows"] = time_next_rows(S, args.steps)
     res["next_rows"].update(time_decode(S, args.steps))
+    res["next_rows"].update(time_slb(args.steps))
     try:
         res["git"] = subprocess.run(["git", "-C", ROOT, "rev-parse", "--short", "HEAD"],
                                     capture_output=True, text=True).stdout.strip() or None

@@ -379,13 +379,20 @@ def l0_longest_prefix(tokens, slots):
     return slot.value, mlen.value
 
 
-def slb_quantize(x: torch.Tensor):
-    """x [n][dim] fp32 (device) -> (int8 codes [n][dim], fp32 scales [n])."""
+def slb_quantize(x: torch.Tensor, out=None):
+    """x [n][dim] fp32 (device) -> (int8 codes [n][dim], fp32 scales [n]); ``out`` may hold
+    preallocated (codes, scales)."""
     if x.dtype != torch.float32 or x.dim() != 2 or not x.is_contiguous() or not x.is_cuda:
         raise NexusError(EINVAL, "x must be a contiguous fp32 [n][dim] device tensor")
     n, dim = x.shape
-    q = torch.empty((n, dim), dtype=torch.int8, device=x.device)
-    s = torch.empty((n,), dtype=torch.float32, device=x.device)
+    if out is None:
+        q = torch.empty((n, dim), dtype=torch.int8, device=x.device)
+        s = torch.empty((n,), dtype=torch.float32, device=x.device)
+    else:
+        q, s = out
+        if (q.dtype != torch.int8 or tuple(q.shape) != (n, dim) or not q.is_contiguous()
+                or s.dtype != torch.float32 or s.numel() != n):
+            raise NexusError(EINVAL, "out must be (int8 [n][dim], fp32 [n]) contiguous tensors")
     _check(lib().nexus_slb_quantize(_ptr(x), n, dim, _ptr(q), _ptr(s), _stream()),
            "nexus_slb_quantize")
     return q, s
