@@ -366,25 +366,14 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a, con
   const SeqPlan sp = plan.seq[b];
   if (sp.n_splits == 1) return;
   const int row = rowg - sp.row_begin;
-  int n_pieces = sp.n_splits;
-  if (plan.stream) {
-    // the workgroups whose runs met this row's task group, in order
-    const int G = a.group;
-    const int tgrp = ((row / kQB) * G + head % G) / kWaves;
-    const int64_t T = plan.stream_tiles, W = plan.units_per_head;
-    const int64_t g0 = sp.vtile_begin + (int64_t)tgrp * sp.vtiles;
-    const int64_t n_real = (task_group_keys(sp.n_past, sp.len, sp.n_tasks, G, tgrp) + 63) / 64;
-    n_pieces = (int)(stream_owner(g0 + n_real - 1, T, W) - stream_owner(g0, T, W) + 1);
-    if (n_pieces == 1) return;   // written by its single workgroup
-  }
   float mmax = -INFINITY;
-  for (int s = 0; s < n_pieces; ++s) {
+  for (int s = 0; s < sp.n_splits; ++s) {
     const int64_t prow = ((int64_t)s * sp.len + row) * a.n_q_heads + head;
     mmax = fmaxf(mmax, a.ws[sp.ml_off + prow * 2]);
   }
   float lsum = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s = 0; s < n_pieces; ++s) {
+  for (int s = 0; s < sp.n_splits; ++s) {
     const int64_t prow = ((int64_t)s * sp.len + row) * a.n_q_heads + head;
     const float2 ml = *reinterpret_cast<const float2 *>(a.ws + sp.ml_off + prow * 2);
     const float w = (ml.x == -INFINITY) ? 0.f : fast_exp2(ml.x - mmax);
@@ -513,89 +502,6 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     }
   }
   const int64_t split_keys = best_sk;
-
-  // Stream plan for the LDS-DMA kernel when every sequence is suffix-like (its task groups
-  // attend to within 10% of the same keys, so reserving the largest group's tile count wastes
-  // little): W workgroups per KV head each take T / W reserved tiles, which removes the partial
-  // last round of the split plan.  Taken when its estimate (same model) is lower.
-  if (p.head_dim == 128 && !p.v_transposed) {
-    bool ok = true;
-    int64_t T = 0;
-    std::vector<int32_t> vt(p.n_seqs);
-    for (int b = 0; b < p.n_seqs && ok; ++b) {
-      const std::vector<int64_t> &wk = tg_keys[b];
-      const AttnSeq &s = p.seqs[b];
-      ok = !wk.empty() && wk.front() * 10 >= wk.back() * 9 && s.n_past + s.len <= kMaxSplitKeys;
-      if (!ok) break;
-      vt[b] = (int32_t)((wk.back() + KT - 1) / KT);
-      T += (int64_t)wk.size() * vt[b];
-    }
-    int64_t W = slots / p.n_kv_heads;
-    if (W > T / 16) W = T / 16;   // at least 16 tiles per workgroup
-    if (ok && W >= 1) {
-      const int64_t per = (T + W - 1) / W;
-      double combine_bytes = 0.0;
-      int64_t max_pieces_all = 1;
-      std::vector<int32_t> maxp(p.n_seqs, 1);
-      int64_t vb = 0;
-      for (int b = 0; b < p.n_seqs; ++b) {
-        const AttnSeq &s = p.seqs[b];
-        const std::vector<int64_t> &wk = tg_keys[b];
-        for (int64_t tg = 0; tg < (int64_t)wk.size(); ++tg) {
-          const int64_t g0 = vb + tg * vt[b];
-          const int64_t n_real = (wk[tg] + KT - 1) / KT;
-          const int64_t np = stream_owner(g0 + n_real - 1, T, W) - stream_owner(g0, T, W) + 1;
-          maxp[b] = (int32_t)std::max<int64_t>(maxp[b], np);
-        }
-        vb += (int64_t)wk.size() * vt[b];
-        max_pieces_all = std::max<int64_t>(max_pieces_all, maxp[b]);
-        if (maxp[b] > 1)
-          combine_bytes += 8.0 * maxp[b] * s.len * p.n_q_heads * (p.head_dim + 2) +
-                           2.0 * s.len * p.n_q_heads * p.head_dim;
-      }
-      // each workgroup meets about per / vtiles + 1 groups, each with its own set-up
-      const int64_t segs = per / std::max<int32_t>(1, vt[0]) + 2;
-      const double est = (double)per * KT + (double)segs * kPieceOverhead;
-      const double cost = est * 0.03 * p.head_dim / 128.0 +
-                          (max_pieces_all > 1 ? combine_bytes / 4.0e6 + 8.0 : 0.0);
-      if (cost < best_cost) {
-        int32_t rows = 0;
-        int64_t ws_floats = 0;
-        vb = 0;
-        for (int b = 0; b < p.n_seqs; ++b) {
-          const AttnSeq &s = p.seqs[b];
-          SeqPlan &sp = plan.seq[b];
-          sp.q_start = s.q_start;
-          sp.len = s.len;
-          sp.n_past = s.n_past;
-          sp.row_begin = rows;
-          sp.first_unit = 0;
-          sp.n_tasks = G * ((s.len + ks.qpw - 1) / ks.qpw);
-          sp.n_splits = maxp[b];
-          sp.split_keys = 0;
-          sp.longest_first = 0;
-          sp.vtiles = vt[b];
-          sp.vtile_begin = vb;
-          vb += (int64_t)tg_keys[b].size() * vt[b];
-          rows += s.len;
-          if (maxp[b] > 1) {
-            plan.any_split = 1;
-            sp.ws_off = ws_floats;
-            ws_floats += (int64_t)maxp[b] * s.len * p.n_q_heads * p.head_dim;
-            sp.ml_off = ws_floats;
-            ws_floats += (int64_t)maxp[b] * s.len * p.n_q_heads * 2;
-          }
-        }
-        plan.stream = 1;
-        plan.stream_tiles = T;
-        plan.units_per_head = (int32_t)W;
-        plan.total_rows = rows;
-        plan.ws_bytes = (size_t)ws_floats * sizeof(float);
-        return true;
-      }
-    }
-  }
-
   int32_t unit = 0, rows = 0;
   int64_t ws_floats = 0;
   for (int b = 0; b < p.n_seqs; ++b) {

@@ -99,11 +99,18 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int j = lane & 31, hh = lane >> 5;
   const int kvh = blockIdx.x % a.n_kv_heads;
+  int unit = blockIdx.x / a.n_kv_heads;
+  int b = 0;
+  while (b + 1 < plan.n_seqs && unit >= plan.seq[b + 1].first_unit) ++b;
+  const SeqPlan sp = plan.seq[b];
+  unit -= sp.first_unit;
+  const int split = unit % sp.n_splits;
+  // prefill-like sequences take their task groups in reverse: later queries see more keys, so
+  // the longest workgroups are dispatched first and the launch does not end on them
+  const int tgrp = sp.longest_first ? (sp.n_tasks + kWaves - 1) / kWaves - 1 - unit / sp.n_splits
+                                    : unit / sp.n_splits;
   const int G = a.group;
 
-  // One piece of work: task group `tgrp` of sequence `sp` over keys [k_begin, min(k_cap, the
-  // group's keys)); its result is the final output (`final_out`) or partial `piece`.
-  auto run = [&](const SeqPlan &sp, int tgrp, int k_begin, int k_cap, int piece, bool final_out) {
   const int task = tgrp * kWaves + wave;
   const bool active = task < sp.n_tasks;
   const int qb = task / G;
@@ -113,7 +120,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
   const int last_task = min(tgrp * kWaves + kWaves - 1, sp.n_tasks - 1);
   const int last_q = min((last_task / G + 1) * kQB, sp.len);
   const int wg_keys = (int)sp.n_past + last_q;
-  const int k_end = min(k_cap, wg_keys);
+  const int k_begin = split * sp.split_keys;
+  const int k_end = min(k_begin + sp.split_keys, wg_keys);
   const int qpos0 = (int)sp.n_past + q0;
   const int n_tiles = k_end > k_begin ? (k_end - k_begin + KT - 1) / KT : 0;
 
@@ -326,7 +334,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
   const float l_tot = sum_halves(l);
   if (!active || q0 + j >= sp.len) return;
   const int row = q0 + j;
-  if (final_out) {
+  if (sp.n_splits == 1) {
     const float inv = 1.0f / l_tot;
     uint16_t *orow = a.out + ((int64_t)(sp.q_start + row) * a.n_q_heads + qhead) * D;
 #pragma unroll
@@ -339,7 +347,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
                   pack_bf16x2(o[db][4 * gq + 2] * inv, o[db][4 * gq + 3] * inv)};
       }
   } else {
-    const int64_t prow = ((int64_t)piece * sp.len + row) * a.n_q_heads + qhead;
+    const int64_t prow = ((int64_t)split * sp.len + row) * a.n_q_heads + qhead;
     float *op = a.ws + sp.ws_off + prow * D;
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
@@ -350,45 +358,6 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
             f32x4{o[db][4 * gq + 0], o[db][4 * gq + 1], o[db][4 * gq + 2], o[db][4 * gq + 3]};
       }
     if (hh == 0) *reinterpret_cast<f32x2 *>(a.ws + sp.ml_off + prow * 2) = f32x2{m_ref, l_tot};
-  }
-  };
-
-  if (!plan.stream) {
-    int unit = blockIdx.x / a.n_kv_heads;
-    int b = 0;
-    while (b + 1 < plan.n_seqs && unit >= plan.seq[b + 1].first_unit) ++b;
-    const SeqPlan &sp = plan.seq[b];
-    unit -= sp.first_unit;
-    const int split = unit % sp.n_splits;
-    // prefill-like sequences take their task groups in reverse: later queries see more keys, so
-    // the longest workgroups are dispatched first and the launch does not end on them
-    const int tgrp = sp.longest_first
-                         ? (sp.n_tasks + kWaves - 1) / kWaves - 1 - unit / sp.n_splits
-                         : unit / sp.n_splits;
-    const int k_begin = split * sp.split_keys;
-    run(sp, tgrp, k_begin, k_begin + sp.split_keys, split, sp.n_splits == 1);
-    return;
-  }
-  // stream plan: this workgroup's run of reserved tiles, cut at task-group boundaries
-  const int64_t T = plan.stream_tiles, W = plan.units_per_head;
-  const int64_t w = blockIdx.x / a.n_kv_heads;
-  const int64_t xe = stream_start(w + 1, T, W);
-  int b = 0;
-  for (int64_t x = stream_start(w, T, W); x < xe;) {
-    while (b + 1 < plan.n_seqs && x >= plan.seq[b + 1].vtile_begin) ++b;
-    const SeqPlan &sp = plan.seq[b];
-    const int tgrp = (int)((x - sp.vtile_begin) / sp.vtiles);
-    const int64_t g0 = sp.vtile_begin + (int64_t)tgrp * sp.vtiles;   // the group's first tile
-    const int64_t seg_end = min(xe, g0 + sp.vtiles);
-    const int n_real =
-        (int)((task_group_keys(sp.n_past, sp.len, sp.n_tasks, G, tgrp) + KT - 1) / KT);
-    const int t0 = (int)(x - g0), t1 = min((int)(seg_end - g0), n_real);
-    if (t0 < t1) {
-      const int64_t w_first = stream_owner(g0, T, W);
-      const int64_t w_last = stream_owner(g0 + n_real - 1, T, W);
-      run(sp, tgrp, t0 * KT, t1 * KT, (int)(w - w_first), w_first == w_last);
-    }
-    x = seg_end;
   }
 }
 

@@ -22,48 +22,16 @@ struct SeqPlan {
   int32_t longest_first;  // dispatch task groups last-first (causal prefill: n_past < len)
   int64_t ws_off;      // float offset of the partial O of this sequence in the workspace
   int64_t ml_off;      // float offset of its (m, l) pairs
-  int32_t vtiles;      // stream plan: key tiles reserved per task group (its largest count)
-  int32_t pad_;
-  int64_t vtile_begin; // stream plan: first reserved tile of this sequence within a KV head
 };
 
-// Two ways to cut a launch into workgroups:
-//   * split plan: unit = (task group, key split); n_splits pieces per task group;
-//   * stream plan (suffix-like sequences): the task groups' key tiles are laid end to end per
-//     KV head, each group reserving `vtiles` tiles (the tiles past its own keys are skipped), and
-//     workgroup w of a head takes reserved tiles [floor(w T / W), floor((w + 1) T / W)), so all
-//     W workgroups per head carry the same work; a group's pieces are the workgroups whose runs
-//     meet its tiles, and n_splits holds the most pieces any group of the sequence has.
 struct AttnPlan {
   SeqPlan seq[kMaxSeqs];
   int32_t n_seqs;
-  int32_t units_per_head;   // workgroups per KV head
+  int32_t units_per_head;
   int32_t total_rows;
   int32_t any_split;
-  int32_t stream;           // 1: stream plan
-  int32_t pad_;
-  int64_t stream_tiles;     // stream plan: reserved tiles per KV head (T)
   size_t ws_bytes;
 };
-
-// Stream plan: first reserved tile of workgroup w, and the workgroup whose run holds tile x.
-__host__ __device__ inline int64_t stream_start(int64_t w, int64_t T, int64_t W) {
-  return w * T / W;
-}
-__host__ __device__ inline int64_t stream_owner(int64_t x, int64_t T, int64_t W) {
-  return ((x + 1) * W - 1) / T;
-}
-
-// Keys a task group attends to: those of its last query (task order: query block major, query
-// head within the group minor, 4 tasks per group).
-__host__ __device__ inline int64_t task_group_keys(int64_t n_past, int len, int n_tasks, int G,
-                                                   int tgrp) {
-  int last_task = tgrp * kWaves + kWaves - 1;
-  if (last_task > n_tasks - 1) last_task = n_tasks - 1;
-  int last_q = (last_task / G + 1) * kQB;
-  if (last_q > len) last_q = len;
-  return n_past + last_q;
-}
 
 struct AttnArgs {
   const uint16_t *q;
