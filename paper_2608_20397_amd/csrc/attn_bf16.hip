@@ -56,11 +56,8 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
   while (b + 1 < plan.n_seqs && unit >= plan.seq[b + 1].first_unit) ++b;
   const SeqPlan sp = plan.seq[b];
   unit -= sp.first_unit;
-  const int split = unit % sp.n_splits;
-  // prefill-like sequences take their task groups in reverse: later queries see more keys, so
-  // the longest workgroups are dispatched first and the launch does not end on them
-  const int tgrp = sp.longest_first ? (sp.n_tasks + kWaves - 1) / kWaves - 1 - unit / sp.n_splits
-                                    : unit / sp.n_splits;
+  const UnitWork uw = unit_work(sp, unit);
+  const int tgrp = uw.tgrp, split = uw.split;
   const int G = a.group;
 
   const int task = tgrp * kWaves + wave;
@@ -73,8 +70,8 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
   const int last_q = min((last_task / G + 1) * kQB, sp.len);
   // positions fit in int32 and element offsets within a layer in uint32 (host-checked)
   const int wg_keys = (int)sp.n_past + last_q;
-  const int k_begin = split * sp.split_keys;
-  const int k_end = min(k_begin + sp.split_keys, wg_keys);
+  const int k_begin = uw.k_begin;
+  const int k_end = min(k_begin + uw.split_keys, wg_keys);
   const int wave_keys = active ? (int)sp.n_past + min(q0 + kQB, sp.len) : 0;
   const int qpos0 = (int)sp.n_past + q0;  // position of this wave's query 0
   const int n_tiles = k_end > k_begin ? (k_end - k_begin + KT - 1) / KT : 0;
@@ -322,7 +319,7 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
   const float l_tot = l + __shfl_xor(l, 32);
   if (!active || q0 + j >= sp.len) return;
   const int row = q0 + j;  // within the sequence
-  if (sp.n_splits == 1) {
+  if (uw.n_splits == 1) {
     const float inv = 1.0f / l_tot;
     uint16_t *orow = a.out + ((int64_t)(sp.q_start + row) * a.n_q_heads + qhead) * D;
 #pragma unroll
@@ -364,16 +361,18 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a, con
   int b = 0;
   while (b + 1 < plan.n_seqs && rowg >= plan.seq[b + 1].row_begin) ++b;
   const SeqPlan sp = plan.seq[b];
-  if (sp.n_splits == 1) return;
   const int row = rowg - sp.row_begin;
+  // the split count of this row's task group (task order: query block major, head minor)
+  const int n_splits = group_splits(sp, ((row / kQB) * a.group + head % a.group) / kWaves);
+  if (n_splits == 1) return;
   float mmax = -INFINITY;
-  for (int s = 0; s < sp.n_splits; ++s) {
+  for (int s = 0; s < n_splits; ++s) {
     const int64_t prow = ((int64_t)s * sp.len + row) * a.n_q_heads + head;
     mmax = fmaxf(mmax, a.ws[sp.ml_off + prow * 2]);
   }
   float lsum = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s = 0; s < sp.n_splits; ++s) {
+  for (int s = 0; s < n_splits; ++s) {
     const int64_t prow = ((int64_t)s * sp.len + row) * a.n_q_heads + head;
     const float2 ml = *reinterpret_cast<const float2 *>(a.ws + sp.ml_off + prow * 2);
     const float w = (ml.x == -INFINITY) ? 0.f : fast_exp2(ml.x - mmax);
@@ -502,6 +501,45 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     }
   }
   const int64_t split_keys = best_sk;
+
+  // Two split classes (one suffix-like sequence): when the units of one split length leave the
+  // last round of workgroup slots partly empty, the first n_a task groups keep a coarse split
+  // that fills whole rounds and the remaining n_b groups take a finer split that fills one last
+  // round, instead of a partial round of full-length units.  Same cost model; slots per KV head.
+  int64_t two_n_a = -1, two_ns_a = 0, two_ns_b = 0;
+  if (p.n_seqs == 1 && !tg_keys[0].empty() && tg_keys[0].front() * 10 >= tg_keys[0].back() * 9) {
+    const AttnSeq &s = p.seqs[0];
+    const int64_t keys = s.n_past + s.len;
+    const int64_t n_tg = (int64_t)tg_keys[0].size();
+    const int64_t slots_h = std::max<int64_t>(1, slots / p.n_kv_heads);
+    const double rows_heads = (double)s.len * p.n_q_heads;
+    auto split_len = [&](int64_t ns) { return seq_split(keys, (keys + ns - 1) / ns); };
+    for (int64_t ns_a = 1; ns_a <= 16; ++ns_a) {
+      const int64_t la = split_len(ns_a);
+      if (la > kMaxSplitKeys || (la < 512 && ns_a > 1)) continue;
+      for (int64_t k = 1; k <= 4; ++k) {
+        const int64_t n_a = std::min(n_tg, k * slots_h / ns_a);
+        const int64_t n_b = n_tg - n_a;
+        if (n_a < 1 || n_b < 1 || n_b > slots_h) continue;
+        const int64_t ns_b = slots_h / n_b;
+        const int64_t lb = split_len(ns_b);
+        if (lb > kMaxSplitKeys || ns_b <= ns_a) continue;
+        const int64_t rounds_a = (n_a * ns_a + slots_h - 1) / slots_h;
+        const double est = (double)rounds_a * (la + kPieceOverhead) + (double)(lb + kPieceOverhead);
+        const double comb = 8.0 * rows_heads * (p.head_dim + 2) *
+                                (double)(n_a * ns_a + n_b * ns_b) / (double)n_tg +
+                            2.0 * rows_heads * p.head_dim;
+        const double cost = est * 0.03 * p.head_dim / 128.0 + comb / 4.0e6 + 8.0;
+        if (cost < best_cost - 1e-9) {
+          best_cost = cost;
+          two_n_a = n_a;
+          two_ns_a = ns_a;
+          two_ns_b = ns_b;
+        }
+      }
+    }
+  }
+
   int32_t unit = 0, rows = 0;
   int64_t ws_floats = 0;
   for (int b = 0; b < p.n_seqs; ++b) {
@@ -524,14 +562,30 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     sp.n_splits = (int32_t)ns;
     sp.split_keys = (int32_t)sk;
     sp.longest_first = s.n_past < s.len ? 1 : 0;
-    unit += n_tg * sp.n_splits;
+    sp.n_tg_a = n_tg;
+    sp.n_splits_b = sp.n_splits;
+    sp.split_keys_b = sp.split_keys;
+    if (two_n_a > 0) {
+      // the two-class cut replaces the single split (one sequence)
+      auto cut = [&](int64_t want, int32_t &n_out, int32_t &k_out) {
+        int64_t kk = (keys + want - 1) / want;
+        kk = (kk + KT - 1) / KT * KT;
+        k_out = (int32_t)kk;
+        n_out = (int32_t)((keys + kk - 1) / kk);
+      };
+      cut(two_ns_a, sp.n_splits, sp.split_keys);
+      cut(two_ns_b, sp.n_splits_b, sp.split_keys_b);
+      sp.n_tg_a = (int32_t)two_n_a;
+    }
+    sp.max_splits = std::max(sp.n_splits, sp.n_splits_b);
+    unit += sp.n_tg_a * sp.n_splits + (n_tg - sp.n_tg_a) * sp.n_splits_b;
     rows += s.len;
-    if (sp.n_splits > 1) {
+    if (sp.max_splits > 1) {
       plan.any_split = 1;
       sp.ws_off = ws_floats;
-      ws_floats += (int64_t)sp.n_splits * s.len * p.n_q_heads * p.head_dim;
+      ws_floats += (int64_t)sp.max_splits * s.len * p.n_q_heads * p.head_dim;
       sp.ml_off = ws_floats;
-      ws_floats += (int64_t)sp.n_splits * s.len * p.n_q_heads * 2;
+      ws_floats += (int64_t)sp.max_splits * s.len * p.n_q_heads * 2;
     }
   }
   plan.units_per_head = unit;

@@ -104,11 +104,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
   while (b + 1 < plan.n_seqs && unit >= plan.seq[b + 1].first_unit) ++b;
   const SeqPlan sp = plan.seq[b];
   unit -= sp.first_unit;
-  const int split = unit % sp.n_splits;
-  // prefill-like sequences take their task groups in reverse: later queries see more keys, so
-  // the longest workgroups are dispatched first and the launch does not end on them
-  const int tgrp = sp.longest_first ? (sp.n_tasks + kWaves - 1) / kWaves - 1 - unit / sp.n_splits
-                                    : unit / sp.n_splits;
+  const UnitWork uw = unit_work(sp, unit);
+  const int tgrp = uw.tgrp, split = uw.split;
   const int G = a.group;
 
   const int task = tgrp * kWaves + wave;
@@ -120,8 +117,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
   const int last_task = min(tgrp * kWaves + kWaves - 1, sp.n_tasks - 1);
   const int last_q = min((last_task / G + 1) * kQB, sp.len);
   const int wg_keys = (int)sp.n_past + last_q;
-  const int k_begin = split * sp.split_keys;
-  const int k_end = min(k_begin + sp.split_keys, wg_keys);
+  const int k_begin = uw.k_begin;
+  const int k_end = min(k_begin + uw.split_keys, wg_keys);
   const int qpos0 = (int)sp.n_past + q0;
   const int n_tiles = k_end > k_begin ? (k_end - k_begin + KT - 1) / KT : 0;
 
@@ -334,7 +331,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
   const float l_tot = sum_halves(l);
   if (!active || q0 + j >= sp.len) return;
   const int row = q0 + j;
-  if (sp.n_splits == 1) {
+  if (uw.n_splits == 1) {
     const float inv = 1.0f / l_tot;
     uint16_t *orow = a.out + ((int64_t)(sp.q_start + row) * a.n_q_heads + qhead) * D;
 #pragma unroll

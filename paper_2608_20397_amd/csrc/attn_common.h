@@ -22,7 +22,50 @@ struct SeqPlan {
   int32_t longest_first;  // dispatch task groups last-first (causal prefill: n_past < len)
   int64_t ws_off;      // float offset of the partial O of this sequence in the workspace
   int64_t ml_off;      // float offset of its (m, l) pairs
+  // Two split classes: the first n_tg_a task groups in dispatch order take n_splits splits of
+  // split_keys keys, the others n_splits_b splits of split_keys_b (a finer cut that fills the
+  // last round of workgroups).  One class: n_tg_a = all groups, class b equal to class a.
+  int32_t n_tg_a;
+  int32_t n_splits_b;
+  int32_t split_keys_b;
+  int32_t max_splits;  // partial slots per row in the workspace: max(n_splits, n_splits_b)
 };
+
+// Work of unit `u` (counted from the sequence's first unit): task group, split, its first key,
+// the split length and the group's split count.
+struct UnitWork {
+  int tgrp, split, k_begin, split_keys, n_splits;
+};
+__device__ __forceinline__ UnitWork unit_work(const SeqPlan &sp, int u) {
+  UnitWork w;
+  const int ua = sp.n_tg_a * sp.n_splits;
+  int di;   // dispatch index of the task group
+  if (u < ua) {
+    di = u / sp.n_splits;
+    w.split = u - di * sp.n_splits;
+    w.split_keys = sp.split_keys;
+    w.n_splits = sp.n_splits;
+  } else {
+    const int ub = u - ua;
+    const int dib = ub / sp.n_splits_b;
+    di = sp.n_tg_a + dib;
+    w.split = ub - dib * sp.n_splits_b;
+    w.split_keys = sp.split_keys_b;
+    w.n_splits = sp.n_splits_b;
+  }
+  // prefill-like sequences take their task groups in reverse: later queries see more keys, so
+  // the longest workgroups are dispatched first and the launch does not end on them
+  const int n_tg = (sp.n_tasks + kWaves - 1) / kWaves;
+  w.tgrp = sp.longest_first ? n_tg - 1 - di : di;
+  w.k_begin = w.split * w.split_keys;
+  return w;
+}
+// Split count of task group `tgrp`.
+__device__ __forceinline__ int group_splits(const SeqPlan &sp, int tgrp) {
+  const int n_tg = (sp.n_tasks + kWaves - 1) / kWaves;
+  const int di = sp.longest_first ? n_tg - 1 - tgrp : tgrp;
+  return di < sp.n_tg_a ? sp.n_splits : sp.n_splits_b;
+}
 
 struct AttnPlan {
   SeqPlan seq[kMaxSeqs];
