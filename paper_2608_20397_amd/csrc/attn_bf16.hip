@@ -422,6 +422,10 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   const int KT = ks.key_tile;
   const int64_t slots = (int64_t)kCUs * ks.wgs_per_cu;
   constexpr int64_t kPieceOverhead = 128;
+  // shortest split in general, and in a launch whose pieces all fit one per CU (a few hundred
+  // queries: latency-bound, where shorter pieces shorten the critical path; measured on the
+  // shallow depths of the depth-adaptive sweep, e.g. 90 queries at 742: 22.8 -> 19.1 us)
+  constexpr int64_t kMinSplitKeys = 512, kMinSplitKeysSmall = 256;
   plan = AttnPlan{};
   plan.n_seqs = p.n_seqs;
   int64_t max_keys = 0;
@@ -455,8 +459,8 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     int64_t sk = (max_keys + ns - 1) / ns;
     sk = (sk + KT - 1) / KT * KT;
     if (sk > kMaxSplitKeys) continue;
-    if (sk < 512 && ns > 1) break;
-    int64_t max_splits = 1, n_full = 0, full_len = 0, max_piece = 0;
+    if (sk < kMinSplitKeysSmall && ns > 1) break;
+    int64_t max_splits = 1, n_full = 0, full_len = 0, max_piece = 0, n_pieces = 0;
     double total = 0.0, combine_bytes = 0.0;
     for (int b = 0; b < p.n_seqs; ++b) {
       const AttnSeq &s = p.seqs[b];
@@ -487,9 +491,11 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
         }
       }
       n_full += full * p.n_kv_heads;
+      n_pieces += pieces * p.n_kv_heads;
       if (!wk.empty()) max_piece = std::max(max_piece, std::min(skb, wk.back()) + kPieceOverhead);
       total += (seq_keys[b] + (double)pieces * kPieceOverhead) * p.n_kv_heads;
     }
+    if (sk < kMinSplitKeys && ns > 1 && n_pieces > kCUs) continue;
     const double rounds_full = (double)((n_full + slots - 1) / slots);
     const double est = std::max({rounds_full * (double)(full_len + kPieceOverhead),
                                  (double)max_piece, total / (double)slots});
@@ -516,7 +522,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     auto split_len = [&](int64_t ns) { return seq_split(keys, (keys + ns - 1) / ns); };
     for (int64_t ns_a = 1; ns_a <= 16; ++ns_a) {
       const int64_t la = split_len(ns_a);
-      if (la > kMaxSplitKeys || (la < 512 && ns_a > 1)) continue;
+      if (la > kMaxSplitKeys || (la < kMinSplitKeys && ns_a > 1)) continue;
       for (int64_t k = 1; k <= 4; ++k) {
         const int64_t n_a = std::min(n_tg, k * slots_h / ns_a);
         const int64_t n_b = n_tg - n_a;

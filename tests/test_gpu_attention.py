@@ -122,6 +122,9 @@ EDGE = {
                                             n_suffix=100, q_scale=1.0, k_scale=1.0, v_scale=1.0),
     "many splits": dict(base_cfg=2, n_ctx=20000, block_len=16, n_user=0, n_suffix=8,
                         n_q_heads=40),
+    # a latency-bound launch (32 workgroups unsplit): its keys are cut into 256-key splits
+    "short splits, 90 queries at 742": dict(base_cfg=2, n_ctx=256, block_len=512, n_user=64,
+                                            n_suffix=90),
     "fp32 transposed V G=2": dict(base_cfg=1, n_ctx=500, block_len=64, n_user=10, n_suffix=40,
                                   n_q_heads=4, n_kv_heads=2, v_layout="transposed", softcap=3.0),
 }
