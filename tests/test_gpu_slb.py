@@ -2,7 +2,8 @@
 for every query the top-k tool indices, their fp32 scores, the top-two margin and the gate
 decision bit for bit (both sides score in fp32 with the same rounding, so every integer
 decision is taken in the same precision).  Registries from 1 to 65536 tools, 1 to 256 queries,
-dims 64..1024, k 1..8, ties from duplicated tools."""
+dims 64..1024 (odd numbers of 64-byte steps too), k 1..8, ties from duplicated tools; both scan
+kernels (up to 16 queries, and the batched one above)."""
 
 import numpy as np
 import pytest
@@ -61,7 +62,9 @@ def test_slb_quantize_and_scan_parity(case):
 
 @pytest.mark.parametrize("n_tools,n_q,dim,k", [(1, 1, 64, 1), (2, 1, 64, 2), (63, 65, 128, 8),
                                                (1025, 7, 192, 5), (4097, 130, 256, 3),
-                                               (3000, 1, 1024, 8)])
+                                               (3000, 1, 1024, 8), (16, 16, 64, 2),
+                                               (17, 17, 64, 2), (700, 40, 192, 4),
+                                               (5000, 33, 320, 2), (40000, 70, 1024, 8)])
 def test_slb_scan_ties_and_ragged(n_tools, n_q, dim, k):
     """Random codes with duplicated tools (equal scores: the lower index first) across tile,
     range and query-block edges."""
