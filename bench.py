@@ -301,10 +301,11 @@ def time_decode(S, reps: int):
       page map), every layer, captured in a HIP graph;
     * decode_b32: 32 sequences of the same depth on private pages (8 layers of synthetic K/V),
       the warm-prefix pool's width;
-    * share_prefix: the first 16384 + 5 tokens of one of those sequences shared with another
-      (1024 pages by reference, 5 slots of each of the 8 layers copied), one launch;
-    * copy_tokens: a 16384-token prefix copied into a third sequence's pages (the copy the
-      paper's arena performs), 8 layers.
+    * share_prefix: the first 16384 + 5 tokens (config 3; fewer in a smaller cache) of one of
+      those sequences shared with another (1024 pages by reference, 5 slots of each of the 8
+      layers copied), one launch;
+    * copy_tokens: a 16384-token prefix (at most the cache) copied into a third sequence's pages
+      (the copy the paper's arena performs), 8 layers.
     GB/s on algorithmic bytes: K and V of every attended key plus q and out (decode); read +
     write of the copied slots (share, copy)."""
     import torch
@@ -347,14 +348,14 @@ def time_decode(S, reps: int):
     # warm-prefix reuse between two sequences of the 32-sequence cache (disjoint pages)
     src, dst = maps[0].contiguous(), maps[1].contiguous()
     slot_bytes = 2 * L8 * H * D * es                      # K and V of one token, all layers
-    n_share = 16384 + 5
+    n_share = min(16384, (n // 16 - 1) * 16) + 5       # whole pages + 5 slots, inside the cache
     # idempotent after its first run: 50 calls per graph
     ms = _graph_time(lambda: N.kv_share_prefix(c32, src, dst, n_share), max(reps, 3), inner=50)
     tail = n_share % 16
     out["share_prefix"] = {"tokens": n_share, "layers": L8, "pages_shared": n_share // 16,
                            "slots_copied": tail, "mean_launch_ms": ms,
                            "bytes_per_launch": 2 * tail * slot_bytes}
-    n_copy = 16384
+    n_copy = min(16384, n)
     dst2 = maps[2].contiguous()
     ms = _graph_time(lambda: N.kv_copy_tokens(c32, src, dst2, 0, n_copy), max(reps, 3))
     nbytes = 2 * n_copy * slot_bytes
