@@ -7,10 +7,12 @@
 //   * rope-append (the redecode writes of Sec. VI-A): freshly computed, un-rotated key token j
 //     is rotated to its absolute position pos0 + j (RoPE, Sec. III-B) and written with its value
 //     row to logical slot offset + j.
-// A workgroup covers kTileTokens tokens of kLayersPerGroup layers, all heads.  It first forms,
-// in fp64, the cosine and sine of every (token, pair) angle it needs (one angle per pair when the
-// rotation is the same for every token) and keeps them in LDS as fp32 head + tail pairs; each
-// thread then streams 16-byte chunks of rows.  HBM-bound.
+// A workgroup covers kTileTokens tokens of one layer, all heads: its source rows are one
+// contiguous run of the block.  Each thread issues the loads of its first kBatch items, then the
+// workgroup forms, in fp64, the cosine and sine of every (token, pair) angle it needs (one angle
+// per pair when the rotation is the same for every token) and keeps them in LDS as fp32 head +
+// tail pairs while those loads are in flight; then the threads rotate and write their items.
+// HBM-bound.
 #include "launch.h"
 #include "rope_math.h"
 
@@ -18,14 +20,17 @@ namespace nexus {
 
 namespace {
 
-constexpr int kTileTokens = 8;        // tokens per workgroup
-constexpr int kLayersPerGroup = 16;   // layers per workgroup
+// 4 tokens per workgroup and one item per thread at a time: with 8 KV heads of 128 bf16 features
+// a workgroup's items are one per thread (config 3, 48 layers: one-pass splice + re-anchor 76 us
+// and rope-append 81 us, against 80 and 87 us with 8 tokens and two items per thread, and 84
+// and 91 us with 8 tokens x 16 layers per workgroup)
+constexpr int kTileTokens = 4;        // tokens per workgroup
 constexpr int kMaxPairsTab = 128;     // head_dim <= 256
+constexpr int kBatch = 1;             // items per thread whose loads are in flight together
 
 }  // namespace
 
-// Thread item = (chunk c of a row, row), rows ordered (layer, head, token) with the token of the
-// tile fastest; a tile always spans kTileTokens token slots and slots past n_tokens idle.
+// Thread item = (chunk c of a row, row), rows in source order (token t of the tile, head h).
 // NEOX: chunk c covers pairs [N c, N c + N): elements [N c, +N) and [D/2 + N c, +N).
 // INTERLEAVED: elements [2 N c, 2 N c + 2 N) = pairs [N c, N c + N).
 template <typename T, bool INTERLEAVED, bool PER_TOKEN>
@@ -35,13 +40,47 @@ __global__ __launch_bounds__(256) void rope_splice_kernel(
     int32_t n_tokens, int32_t n_heads, FastDiv div_heads, int32_t head_dim, uint32_t tpr_shift,
     int32_t n_phys_pages, int64_t angle0, double base) {
   constexpr int N = Pack<T>::N;
-  constexpr int kBatch = 4;                       // items whose loads are in flight together
   __shared__ float cs_tab[4][PER_TOKEN ? kTileTokens : 1][kMaxPairsTab];
   const int j0 = blockIdx.x * kTileTokens;
-  const int l0 = blockIdx.y * kLayersPerGroup;
+  const int l = blockIdx.y;
   const int n_tok = min(kTileTokens, n_tokens - j0);
-  const int n_lay = min(kLayersPerGroup, n_layers - l0);
   const int n_pairs = head_dim / 2;
+  const uint32_t items = (uint32_t)(n_tok * n_heads) << tpr_shift;
+  const uint32_t tpr_mask = (1u << tpr_shift) - 1;
+  const int64_t src0 = ((int64_t)l * n_tokens + j0) * n_heads * head_dim;   // the tile's rows
+
+  struct Item {
+    u32x4 ka, kb, va, vb;
+    int64_t drow;
+    int t, c;
+  };
+  // loads of item it (clamped to the last item: always a valid row)
+  auto load = [&](uint32_t it_raw, Item &x) {
+    const uint32_t it = it_raw < items ? it_raw : items - 1;
+    const int c = it & tpr_mask;
+    const uint32_t r = it >> tpr_shift;                    // t * n_heads + h
+    const int t = fdiv(r, div_heads);
+    const int h = r - t * n_heads;
+    const int64_t srow = src0 + (int64_t)r * head_dim;
+    const int64_t tok = offset + j0 + t;
+    const int64_t page = (uint32_t)map[tok >> kPageShift];
+    x.drow = ((((int64_t)l * n_phys_pages + page) * n_heads + h) * kPage + (tok & (kPage - 1))) *
+             head_dim;
+    x.t = t;
+    x.c = c;
+    const int ea = INTERLEAVED ? 2 * N * c : N * c;             // first element of each load
+    const int eb = INTERLEAVED ? 2 * N * c + N : n_pairs + N * c;
+    x.ka = *reinterpret_cast<const u32x4 *>(src_k + srow + ea);
+    x.kb = *reinterpret_cast<const u32x4 *>(src_k + srow + eb);
+    if (src_v != nullptr) {
+      x.va = *reinterpret_cast<const u32x4 *>(src_v + srow + ea);
+      x.vb = *reinterpret_cast<const u32x4 *>(src_v + srow + eb);
+    }
+  };
+  Item cur[kBatch];
+#pragma unroll
+  for (int u = 0; u < kBatch; ++u) load(threadIdx.x + u * blockDim.x, cur[u]);
+
   const int n_ang = (PER_TOKEN ? n_tok : 1) * n_pairs;
   for (int x = threadIdx.x; x < n_ang; x += blockDim.x) {
     const int t = x / n_pairs, i = x - t * n_pairs;
@@ -50,54 +89,23 @@ __global__ __launch_bounds__(256) void rope_splice_kernel(
     pair_cs(d, base, i, head_dim, cs_tab[0][t][i], cs_tab[1][t][i], cs_tab[2][t][i],
             cs_tab[3][t][i]);
   }
-  __syncthreads();
+  // LDS-only barrier: the item loads above stay in flight
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 
-  const uint32_t items = (uint32_t)(n_lay * n_heads * kTileTokens) << tpr_shift;
-  const uint32_t tpr_mask = (1u << tpr_shift) - 1;
   for (uint32_t it0 = threadIdx.x; it0 < items; it0 += kBatch * blockDim.x) {
-    u32x4 ka[kBatch], kb[kBatch], va[kBatch], vb[kBatch];
-    int64_t drow[kBatch];
-    int tt[kBatch], cc[kBatch];
-    bool ok[kBatch];
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
-      const uint32_t it = it0 + u * blockDim.x;
-      const int c = it & tpr_mask;
-      const uint32_t r = it >> tpr_shift;
-      const int t = r % kTileTokens;
-      const uint32_t lh = r / kTileTokens;
-      const uint32_t lq = fdiv(lh, div_heads);
-      const int h = lh - lq * n_heads;
-      const int l = l0 + lq;
-      const int j = j0 + t;
-      ok[u] = it < items && t < n_tok;
-      tt[u] = PER_TOKEN ? t : 0;
-      cc[u] = c;
-      drow[u] = 0;
-      if (!ok[u]) continue;
-      const int64_t srow = (((int64_t)l * n_tokens + j) * n_heads + h) * head_dim;
-      const int64_t tok = offset + j;
-      const int64_t page = (uint32_t)map[tok >> kPageShift];
-      drow[u] = ((((int64_t)l * n_phys_pages + page) * n_heads + h) * kPage + (tok & (kPage - 1))) *
-                head_dim;
-      const int ea = INTERLEAVED ? 2 * N * c : N * c;            // first element of each load
-      const int eb = INTERLEAVED ? 2 * N * c + N : n_pairs + N * c;
-      ka[u] = *reinterpret_cast<const u32x4 *>(src_k + srow + ea);
-      kb[u] = *reinterpret_cast<const u32x4 *>(src_k + srow + eb);
-      if (src_v != nullptr) {
-        va[u] = *reinterpret_cast<const u32x4 *>(src_v + srow + ea);
-        vb[u] = *reinterpret_cast<const u32x4 *>(src_v + srow + eb);
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      if (!ok[u]) continue;
-      const int c = cc[u];
+      if (it0 + u * blockDim.x >= items) continue;
+      const Item &x0 = cur[u];
+      const int c = x0.c;
+      const int tt = PER_TOKEN ? x0.t : 0;
       const int ea = INTERLEAVED ? 2 * N * c : N * c;
       const int eb = INTERLEAVED ? 2 * N * c + N : n_pairs + N * c;
       float x[2 * N], a[N], b[N];
-      Pack<T>::unpack(ka[u], x);
-      Pack<T>::unpack(kb[u], x + N);
+      Pack<T>::unpack(x0.ka, x);
+      Pack<T>::unpack(x0.kb, x + N);
 #pragma unroll
       for (int e = 0; e < N; ++e) {
         a[e] = INTERLEAVED ? x[2 * e] : x[e];
@@ -106,10 +114,10 @@ __global__ __launch_bounds__(256) void rope_splice_kernel(
       float ch[N], cl[N], sh[N], sl[N];
 #pragma unroll
       for (int e = 0; e < N; ++e) {
-        ch[e] = cs_tab[0][tt[u]][N * c + e];
-        cl[e] = cs_tab[1][tt[u]][N * c + e];
-        sh[e] = cs_tab[2][tt[u]][N * c + e];
-        sl[e] = cs_tab[3][tt[u]][N * c + e];
+        ch[e] = cs_tab[0][tt][N * c + e];
+        cl[e] = cs_tab[1][tt][N * c + e];
+        sh[e] = cs_tab[2][tt][N * c + e];
+        sl[e] = cs_tab[3][tt][N * c + e];
       }
       rotate<N>(a, b, ch, cl, sh, sl);
 #pragma unroll
@@ -122,21 +130,25 @@ __global__ __launch_bounds__(256) void rope_splice_kernel(
           x[N + e] = b[e];
         }
       }
-      *reinterpret_cast<u32x4 *>(ck + drow[u] + ea) = Pack<T>::pack(x);
-      *reinterpret_cast<u32x4 *>(ck + drow[u] + eb) = Pack<T>::pack(x + N);
+      *reinterpret_cast<u32x4 *>(ck + x0.drow + ea) = Pack<T>::pack(x);
+      *reinterpret_cast<u32x4 *>(ck + x0.drow + eb) = Pack<T>::pack(x + N);
       if (src_v != nullptr) {
-        *reinterpret_cast<u32x4 *>(cv + drow[u] + ea) = va[u];
-        *reinterpret_cast<u32x4 *>(cv + drow[u] + eb) = vb[u];
+        *reinterpret_cast<u32x4 *>(cv + x0.drow + ea) = x0.va;
+        *reinterpret_cast<u32x4 *>(cv + x0.drow + eb) = x0.vb;
       }
     }
+    if (it0 + kBatch * blockDim.x < items) {
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) load(it0 + (kBatch + u) * blockDim.x, cur[u]);
+    }
   }
+  (void)n_layers;
 }
 
 hipError_t launch_rope_splice(const RopeSpliceLaunch &p, hipStream_t stream) {
   // V of a transposed cache goes through the splice kernel's transposing path
   const bool v_rows = !p.v_transposed;
-  const dim3 grid((p.n_tokens + kTileTokens - 1) / kTileTokens,
-                  (p.n_layers + kLayersPerGroup - 1) / kLayersPerGroup);
+  const dim3 grid((p.n_tokens + kTileTokens - 1) / kTileTokens, p.n_layers);
   const uint32_t tpr = (uint32_t)(p.head_dim / 2 / (16 / p.dtype_bytes));
   uint32_t shift = 0;
   while ((1u << shift) < tpr) ++shift;
