@@ -315,8 +315,8 @@ nexus_status nexus_l0_longest_prefix(const int32_t *tokens, int32_t n_tokens,
  *   The paper calibrates tau = 0.0136 (the 20th percentile of adversarial-pair margins).
  * workspace: nexus_slb_scan_workspace() bytes (NULL allowed when 0).  Checks: non-NULL arrays,
  * n_tools > 0, n_queries > 0, 1 <= k <= 8, finite tau (NEXUS_EINVAL); dim a multiple of 64 in
- * [64, 1024] (NEXUS_ESHAPE).  Queries are processed in blocks of 64 on int8 MFMA, so a batch of
- * queries costs little more than one.
+ * [64, 1024] (NEXUS_ESHAPE).  Up to 16 queries share one pass over the tool rows; larger batches
+ * go in blocks of 64 queries on int8 MFMA, so a batch costs far less than its queries one by one.
  */
 nexus_status nexus_slb_quantize(const float *x, int32_t n, int32_t dim, int8_t *q, float *scale,
                                 void *stream);
