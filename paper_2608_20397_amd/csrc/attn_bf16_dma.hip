@@ -293,6 +293,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
       }
       const float nm = (m_ref == -INFINITY) ? 0.f : -m_ref;
       const char *vl = vbuf(P);
+      // The softmax of S(t) and O += V P run at a raised wave priority: of the two waves that
+      // share a SIMD, the one in this phase issues first, so its exponentials and PV MFMAs
+      // interleave with the other wave's S^T MFMAs instead of queueing behind them (measured
+      // about 4% faster per call at config 3; results are bit-identical).
+      __builtin_amdgcn_s_setprio(2);
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
@@ -315,6 +320,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
           }
         }
     }
+    __builtin_amdgcn_s_setprio(0);
     // pages for the next iteration's DMA (the LDS read overlaps the wait below)
     pv = pk;
     if (t + 3 < n_tiles && full(t + 3)) pk = page_of(t + 3);
