@@ -396,6 +396,9 @@ __global__ __launch_bounds__(256, 2) void slb_block_kernel(SlbArgs a) {
       }
     }
     if (c != n_chunks - 1) return;
+    // the candidate pass runs at a raised wave priority, so that its list upkeep interleaves
+    // with the other wave's MFMA chains (about 4% faster at 65536 tools x 256 queries)
+    __builtin_amdgcn_s_setprio(2);
     // the block's 64 x 64 scores: a candidate that does not beat its column's floor (at most
     // the column's KT-th best) cannot be among the column's best KT and is dropped
     const int tb = 64 * (wave + kWaves * j);                   // block start within the range
@@ -415,6 +418,7 @@ __global__ __launch_bounds__(256, 2) void slb_block_kernel(SlbArgs a) {
     }
 #pragma unroll
     for (int sb = 0; sb < NSB; ++sb) floor_key[sb] = column_floor<KT>(best[sb]);
+    __builtin_amdgcn_s_setprio(0);
   };
   if (total > 0) {
     Chunk b0, b1;
