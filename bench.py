@@ -11,7 +11,7 @@ over a 17472-token cache.
 Prints one JSON line.  ``value`` is the whole-step attention throughput (algorithmic attention
 FLOPs per step / step time, TFLOP/s); ``roofline`` reports the attention kernel against the bf16
 MFMA peak and ``roofline_hbm`` the splice and re-anchor kernels against HBM bandwidth, all on
-algorithmic work.  ``cpu_baseline`` times the fp64 oracle on a bounded sample of
+algorithmic work (the bytes or FLOPs the operation itself defines).  ``cpu_baseline`` times the fp64 oracle on a bounded sample of
 the same workload on the host cores.
 """
 
@@ -541,7 +541,7 @@ def main():
                          "scale of the FETCH_SIZE / WRITE_SIZE counters), then exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on one GPU only (no multi-GPU path); use --gpus 1",
+        print("bench.py: runs on one GPU only (the library has no multi-GPU path); use --gpus 1",
               file=sys.stderr)
         sys.exit(2)
 
