@@ -66,7 +66,8 @@ typedef enum nexus_rope_style { NEXUS_ROPE_NEOX = 0, NEXUS_ROPE_INTERLEAVED = 1 
  *   base_pos    RoPE anchor of the keys currently stored in `k` (m0 when freshly compiled);
  *               nexus_rephase_k updates it.
  *   rope_base   b of theta_i = b^(-2i/D); rope_style as above.
- * head_dim must be even; bf16 blocks need head_dim % 16 == 0, f32 blocks head_dim % 8 == 0.
+ * head_dim is a power of two, 16..1024 for bf16 and 8..1024 for f32 (rows move as a power-of-two
+ * number of 16-byte chunks); anything else is NEXUS_ESHAPE.  Caches take the same head_dim.
  */
 typedef struct nexus_block {
   void *k;

@@ -121,6 +121,11 @@ def test_splice_validation_fails_closed():
     assert L.nexus_splice_pages(C.byref(bc), C.byref(pt), C.byref(block), 0, s) == N.ESHAPE
     bc = N.CKvCache.from_buffer_copy(cache); bc.head_dim = 60; block2 = N.CBlock.from_buffer_copy(block); block2.head_dim = 60
     assert L.nexus_splice_pages(C.byref(bc), C.byref(pt), C.byref(block2), 0, s) == N.ESHAPE
+    # head_dim must be a power of two: 96 and 48 pass the per-chunk divisibility checks
+    for hd in (96, 48):
+        bc = N.CKvCache.from_buffer_copy(cache); bc.head_dim = hd
+        block2 = N.CBlock.from_buffer_copy(block); block2.head_dim = hd
+        assert L.nexus_splice_pages(C.byref(bc), C.byref(pt), C.byref(block2), 0, s) == N.ESHAPE
 
 
 def test_rephase_validation_and_identity():
