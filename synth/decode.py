@@ -150,7 +150,12 @@ def written_slots(wl: DecodeWorkload, maps: np.ndarray) -> np.ndarray:
 def decode_host_case(case: int, layers=None) -> DecodeHostCase:
     """Host draws of one decode case (all pool pages are drawn; unwritten slots get the NaN
     sentinel)."""
-    wl = decode_workload(case)
+    return decode_host_case_wl(decode_workload(case), layers)
+
+
+def decode_host_case_wl(wl: DecodeWorkload, layers=None) -> DecodeHostCase:
+    """Host draws of any decode workload record (seeds from its ``case`` slot)."""
+    case = wl.case
     layers = list(range(wl.n_layers)) if layers is None else list(layers)
     H, D, NPP = wl.n_kv_heads, wl.head_dim, wl.n_phys_pages
     maps = page_maps(wl)
