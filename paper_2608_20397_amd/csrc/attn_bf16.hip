@@ -51,12 +51,10 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
   const int wave = tid >> 6, lane = tid & 63;
   const int j = lane & 31, hh = lane >> 5;
   const int kvh = blockIdx.x % a.n_kv_heads;
-  int unit = blockIdx.x / a.n_kv_heads;
-  int b = 0;
-  while (b + 1 < plan.n_seqs && unit >= plan.seq[b + 1].first_unit) ++b;
+  const UnitLoc loc = locate_unit(plan, blockIdx.x / a.n_kv_heads);
+  const int b = loc.seq;
+  const UnitWork uw = loc.w;
   const SeqPlan sp = plan.seq[b];
-  unit -= sp.first_unit;
-  const UnitWork uw = unit_work(sp, unit);
   const int tgrp = uw.tgrp, split = uw.split;
   const int G = a.group;
 
@@ -453,9 +451,12 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
       seq_keys[b] += (double)tg_keys[b][tg];
     }
   }
+  // several sequences: one split length for all, units range by range (AttnPlan); the split
+  // count candidates below keep the ranges within kMaxRanges
+  const bool range_major = p.n_seqs > 1;
   int64_t best_sk = kMaxSplitKeys;
   double best_cost = 1e300;
-  for (int ns = 1; ns <= 64; ++ns) {
+  for (int ns = 1; ns <= kMaxRanges; ++ns) {
     int64_t sk = (max_keys + ns - 1) / ns;
     sk = (sk + KT - 1) / KT * KT;
     if (sk > kMaxSplitKeys) continue;
@@ -466,7 +467,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
       const AttnSeq &s = p.seqs[b];
       const std::vector<int64_t> &wk = tg_keys[b];
       const int64_t keys = s.n_past + s.len;
-      const int64_t skb = seq_split(keys, sk);
+      const int64_t skb = range_major ? sk : seq_split(keys, sk);
       const int64_t nsb = (keys + skb - 1) / skb;
       max_splits = std::max(max_splits, nsb);
       if (nsb > 1)
@@ -561,8 +562,9 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     const int64_t keys = s.n_past + s.len;
     int64_t ns = (keys + split_keys - 1) / split_keys;
     if (ns < 1) ns = 1;
-    // balance the splits: equal key counts rounded to the tile
-    int64_t sk = (keys + ns - 1) / ns;
+    // balance the splits: equal key counts rounded to the tile (one sequence), or the launch's
+    // common split length (several: aligned key ranges)
+    int64_t sk = range_major ? split_keys : (keys + ns - 1) / ns;
     sk = (sk + KT - 1) / KT * KT;
     ns = (keys + sk - 1) / sk;
     sp.n_splits = (int32_t)ns;
@@ -597,6 +599,29 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   plan.units_per_head = unit;
   plan.total_rows = rows;
   plan.ws_bytes = (size_t)ws_floats * sizeof(float);
+  if (range_major) {
+    // sequences by decreasing split count (the sequences of range r are then a prefix), their
+    // task-group prefix sums, and the first unit of each range
+    plan.range_major = 1;
+    for (int b = 0; b < p.n_seqs; ++b) plan.order[b] = b;
+    std::stable_sort(plan.order, plan.order + p.n_seqs, [&](int x, int y) {
+      return plan.seq[x].n_splits > plan.seq[y].n_splits;
+    });
+    plan.tg_prefix[0] = 0;
+    for (int i = 0; i < p.n_seqs; ++i) {
+      const SeqPlan &sp = plan.seq[plan.order[i]];
+      plan.tg_prefix[i + 1] = plan.tg_prefix[i] + (sp.n_tasks + kWaves - 1) / kWaves;
+    }
+    plan.n_ranges = plan.seq[plan.order[0]].n_splits;
+    if (plan.n_ranges > kMaxRanges) return false;
+    plan.range_first_unit[0] = 0;
+    for (int r = 0; r < plan.n_ranges; ++r) {
+      int m = 0;
+      while (m < p.n_seqs && plan.seq[plan.order[m]].n_splits > r) ++m;
+      plan.range_first_unit[r + 1] = plan.range_first_unit[r] + plan.tg_prefix[m];
+    }
+    if (plan.range_first_unit[plan.n_ranges] != plan.units_per_head) return false;
+  }
   return true;
 }
 

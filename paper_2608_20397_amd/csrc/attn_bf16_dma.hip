@@ -99,12 +99,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int j = lane & 31, hh = lane >> 5;
   const int kvh = blockIdx.x % a.n_kv_heads;
-  int unit = blockIdx.x / a.n_kv_heads;
-  int b = 0;
-  while (b + 1 < plan.n_seqs && unit >= plan.seq[b + 1].first_unit) ++b;
+  const UnitLoc loc = locate_unit(plan, blockIdx.x / a.n_kv_heads);
+  const int b = loc.seq;
+  const UnitWork uw = loc.w;
   const SeqPlan sp = plan.seq[b];
-  unit -= sp.first_unit;
-  const UnitWork uw = unit_work(sp, unit);
   const int tgrp = uw.tgrp, split = uw.split;
   const int G = a.group;
 

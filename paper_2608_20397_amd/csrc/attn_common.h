@@ -67,6 +67,13 @@ __device__ __forceinline__ int group_splits(const SeqPlan &sp, int tgrp) {
   return di < sp.n_tg_a ? sp.n_splits : sp.n_splits_b;
 }
 
+// Several sequences share the cache prefix (blocks spliced into one context): their units are
+// taken key range by key range, so that the workgroups resident together read the same keys.
+// Split r of every sequence covers keys [r * split_keys, (r + 1) * split_keys) (one split
+// length for all); range r holds, for each sequence with more than r splits (a prefix of the
+// sequences ordered by decreasing key count), all its task groups.
+constexpr int kMaxRanges = 64;
+
 struct AttnPlan {
   SeqPlan seq[kMaxSeqs];
   int32_t n_seqs;
@@ -74,7 +81,51 @@ struct AttnPlan {
   int32_t total_rows;
   int32_t any_split;
   size_t ws_bytes;
+  int32_t range_major;                        // 0: units sequence by sequence (first_unit)
+  int32_t n_ranges;
+  int32_t range_first_unit[kMaxRanges + 1];   // first unit of each key range
+  int32_t order[kMaxSeqs];                    // sequences by decreasing key count
+  int32_t tg_prefix[kMaxSeqs + 1];            // task groups of order[0 .. i - 1]
 };
+
+// Sequence and work of unit `unit` of a launch (one KV head's units).
+struct UnitLoc {
+  int seq;
+  UnitWork w;
+};
+__device__ __forceinline__ UnitLoc locate_unit(const AttnPlan &plan, int unit) {
+  UnitLoc loc;
+  if (!plan.range_major) {
+    int b = 0;
+    while (b + 1 < plan.n_seqs && unit >= plan.seq[b + 1].first_unit) ++b;
+    loc.seq = b;
+    loc.w = unit_work(plan.seq[b], unit - plan.seq[b].first_unit);
+    return loc;
+  }
+  int lo = 0, hi = plan.n_ranges;             // range_first_unit[lo] <= unit < [hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (unit >= plan.range_first_unit[mid]) lo = mid;
+    else hi = mid;
+  }
+  const int local = unit - plan.range_first_unit[lo];
+  int i0 = 0, i1 = plan.n_seqs;               // tg_prefix[i0] <= local < tg_prefix[i1]
+  while (i1 - i0 > 1) {
+    const int mid = (i0 + i1) >> 1;
+    if (local >= plan.tg_prefix[mid]) i0 = mid;
+    else i1 = mid;
+  }
+  const int b = plan.order[i0];
+  const int di = local - plan.tg_prefix[i0];
+  const int n_tg = (plan.seq[b].n_tasks + kWaves - 1) / kWaves;
+  loc.seq = b;
+  loc.w.tgrp = plan.seq[b].longest_first ? n_tg - 1 - di : di;
+  loc.w.split = lo;
+  loc.w.split_keys = plan.seq[b].split_keys;
+  loc.w.n_splits = plan.seq[b].n_splits;
+  loc.w.k_begin = lo * plan.seq[b].split_keys;
+  return loc;
+}
 
 struct AttnArgs {
   const uint16_t *q;
