@@ -113,8 +113,15 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
   constexpr int V_PER_T_T = V_ITEMS_T / 256;
   static_assert(K_ITEMS >= 1 && KT * KCH % 256 == 0, "tile too small");
   static_assert(V_PER_T_RM == 1 || VT, "one V group per thread");
-  u32x4 kreg[K_ITEMS];
-  u32x4 vreg[VT ? V_PER_T_T : 4];
+  // staging registers of the tiles on their way to LDS: with head_dim 256 (one workgroup per
+  // CU, registers to spare) two tiles are in flight, else one
+  constexpr int NPRE = D >= 256 ? 2 : 1;
+  constexpr int VN = VT ? V_PER_T_T : 4;
+  struct Stage {
+    u32x4 k[K_ITEMS];
+    u32x4 v[VN];
+  };
+  Stage stg[NPRE];
 
   // K: thread owns chunk kc of keys kkey[i]
   const int kc = tid % KCH;
@@ -130,7 +137,7 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
   // addresses are a uniform base plus a 32-bit unsigned byte offset.
   const char *kbytes = reinterpret_cast<const char *>(kbase);
   const char *vbytes = reinterpret_cast<const char *>(VT ? vtbase : vbase);
-  auto load_tile = [&](int it) {
+  auto load_tile = [&](int it, Stage &sg) {
     const int kt = k_begin + it * KT;
     const int tl = k_end - 1;
 #pragma unroll
@@ -139,7 +146,7 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
       const uint32_t t = (uint32_t)min(kt + key, tl);
       const uint32_t page = (uint32_t)pg[(t >> kPageShift) - pg0];
       const uint32_t off = (__umul24(page, pstride) + (t & (kPage - 1)) * D + kc * 8) * 2u;
-      kreg[i] = *reinterpret_cast<const u32x4 *>(kbytes + off);
+      sg.k[i] = *reinterpret_cast<const u32x4 *>(kbytes + off);
     }
     if constexpr (!VT) {
       if (kAllOwnV || v_owner) {
@@ -149,7 +156,7 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const uint32_t t = (uint32_t)min(kt + 4 * vg4 + e, tl);
-          vreg[e] = *reinterpret_cast<const u32x4 *>(vbytes + (base + (t & (kPage - 1)) * D) * 2u);
+          sg.v[e] = *reinterpret_cast<const u32x4 *>(vbytes + (base + (t & (kPage - 1)) * D) * 2u);
         }
       }
     } else {
@@ -169,18 +176,18 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
           for (int e = 0; e < 8; ++e)
             if (e >= nvalid) val[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
         }
-        vreg[i] = val;
+        sg.v[i] = val;
       }
     }
   };
 
-  auto store_tile = [&](int buf) {
+  auto store_tile = [&](int buf, const Stage &sg) {
     uint16_t *ks = Ks[buf];
     uint16_t *vs = Vs[buf];
 #pragma unroll
     for (int i = 0; i < K_ITEMS; ++i) {
       const int key = (tid + 256 * i) / KCH;
-      *reinterpret_cast<u32x4 *>(ks + key * D + ((kc ^ (key & KSW)) * 8)) = kreg[i];
+      *reinterpret_cast<u32x4 *>(ks + key * D + ((kc ^ (key & KSW)) * 8)) = sg.k[i];
     }
     if constexpr (!VT) {
       if (kAllOwnV || v_owner) {
@@ -191,8 +198,8 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
           const int wi = dd >> 1;
           // gather feature dd of the 4 tokens: low or high halves of word wi
           const uint32_t sel = (dd & 1) ? 0x07060302u : 0x05040100u;
-          const uint32_t lo = __builtin_amdgcn_perm(vreg[1][wi], vreg[0][wi], sel);
-          const uint32_t hi = __builtin_amdgcn_perm(vreg[3][wi], vreg[2][wi], sel);
+          const uint32_t lo = __builtin_amdgcn_perm(sg.v[1][wi], sg.v[0][wi], sel);
+          const uint32_t hi = __builtin_amdgcn_perm(sg.v[3][wi], sg.v[2][wi], sel);
           const int d = 8 * vdc + dd;
           *reinterpret_cast<u32x2 *>(vs + d * KT + ((cc ^ vt_swz<VSW>(d)) * 8) + half * 4) =
               u32x2{lo, hi};
@@ -208,7 +215,7 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
           const int k4 = 8 * grp + 4 * hf;
           const int pos = (k4 & ~15) | vt_pos(k4 & 15);
           const int cc = pos >> 3, half = (pos >> 2) & 1;
-          const u32x2 piece = hf ? u32x2{vreg[i][2], vreg[i][3]} : u32x2{vreg[i][0], vreg[i][1]};
+          const u32x2 piece = hf ? u32x2{sg.v[i][2], sg.v[i][3]} : u32x2{sg.v[i][0], sg.v[i][1]};
           *reinterpret_cast<u32x2 *>(vs + d * KT + ((cc ^ vt_swz<VSW>(d)) * 8) + half * 4) = piece;
         }
       }
@@ -218,14 +225,17 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
   const float c_scale = CAP ? 1.0f : a.scale_log2;   // raw score -> log2 units
   const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
 
-  // ---- pipeline: tile t is in LDS buffer t & 1 while tile t + 1 waits in registers
+  // ---- pipeline: tile t is in LDS buffer t & 1 while tiles t + 1 .. t + NPRE wait in
+  // registers; tile j is staged in stg[j % NPRE]
   if (n_tiles > 0) {
-    load_tile(0);
-    store_tile(0);
-    if (n_tiles > 1) load_tile(1);
+    load_tile(0, stg[0]);
+    store_tile(0, stg[0]);
+#pragma unroll
+    for (int j = 1; j <= NPRE; ++j)
+      if (j < n_tiles) load_tile(j, stg[j % NPRE]);
   }
   __syncthreads();
-  for (int it = 0; it < n_tiles; ++it) {
+  auto step = [&](int it, Stage &nxt) {
     const int kt = k_begin + it * KT;
     const uint16_t *ks = Ks[it & 1];
     const uint16_t *vs = Vs[it & 1];
@@ -308,9 +318,18 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
           }
         }
     }
-    if (it + 1 < n_tiles) store_tile((it + 1) & 1);
-    if (it + 2 < n_tiles) load_tile(it + 2);
+    // tile it + 1 leaves its registers for LDS, which then take tile it + 1 + NPRE
+    if (it + 1 < n_tiles) store_tile((it + 1) & 1, nxt);
+    if (it + 1 + NPRE < n_tiles) load_tile(it + 1 + NPRE, nxt);
     __syncthreads();
+  };
+  if constexpr (NPRE == 1) {
+    for (int it = 0; it < n_tiles; ++it) step(it, stg[0]);
+  } else {
+    for (int it = 0; it < n_tiles; it += 2) {
+      step(it, stg[1]);
+      if (it + 1 < n_tiles) step(it + 1, stg[NPRE - 2]);
+    }
   }
 
   // ---- epilogue
