@@ -365,6 +365,8 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
 
 // Fixed-order merge of the split partials: m = max m_s, w_s = 2^(m_s - m),
 // out = sum_s w_s O_s / sum_s w_s l_s.  One thread per 4 output features.
+constexpr int kCombinePre = 8;   // splits whose partials the combine loads up front
+
 template <int D>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a, const AttnPlan plan) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -382,23 +384,49 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a, con
   // the split count of this row's task group (task order: query block major, head minor)
   const int n_splits = group_splits(sp, ((row / kQB) * a.group + head % a.group) / kWaves);
   if (n_splits == 1) return;
+  const int64_t pstep = (int64_t)sp.len * a.n_q_heads;         // partial rows per split
+  const int64_t prow0 = (int64_t)row * a.n_q_heads + head;
   float mmax = -INFINITY;
-  for (int s = 0; s < n_splits; ++s) {
-    const int64_t prow = ((int64_t)s * sp.len + row) * a.n_q_heads + head;
-    mmax = fmaxf(mmax, a.ws[sp.ml_off + prow * 2]);
-  }
   float lsum = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s = 0; s < n_splits; ++s) {
-    const int64_t prow = ((int64_t)s * sp.len + row) * a.n_q_heads + head;
-    const float2 ml = *reinterpret_cast<const float2 *>(a.ws + sp.ml_off + prow * 2);
-    const float w = (ml.x == -INFINITY) ? 0.f : fast_exp2(ml.x - mmax);
-    lsum += w * ml.y;
-    const float4 ov = *reinterpret_cast<const float4 *>(a.ws + sp.ws_off + prow * D + 4 * d4);
-    acc.x += w * ov.x;
-    acc.y += w * ov.y;
-    acc.z += w * ov.z;
-    acc.w += w * ov.w;
+  if (n_splits <= kCombinePre) {
+    // every split's (m, l) and O loaded up front (splits past n_splits re-read the last one
+    // and weigh 0), then merged in split order: one round trip instead of one per split
+    float2 ml[kCombinePre];
+    float4 ov[kCombinePre];
+#pragma unroll
+    for (int s = 0; s < kCombinePre; ++s) {
+      const int64_t prow = min(s, n_splits - 1) * pstep + prow0;
+      ml[s] = *reinterpret_cast<const float2 *>(a.ws + sp.ml_off + prow * 2);
+      ov[s] = *reinterpret_cast<const float4 *>(a.ws + sp.ws_off + prow * D + 4 * d4);
+    }
+#pragma unroll
+    for (int s = 0; s < kCombinePre; ++s)
+      if (s < n_splits) mmax = fmaxf(mmax, ml[s].x);
+#pragma unroll
+    for (int s = 0; s < kCombinePre; ++s) {
+      if (s >= n_splits) break;
+      const float w = (ml[s].x == -INFINITY) ? 0.f : fast_exp2(ml[s].x - mmax);
+      lsum += w * ml[s].y;
+      acc.x += w * ov[s].x;
+      acc.y += w * ov[s].y;
+      acc.z += w * ov[s].z;
+      acc.w += w * ov[s].w;
+    }
+  } else {
+    for (int s = 0; s < n_splits; ++s)
+      mmax = fmaxf(mmax, a.ws[sp.ml_off + (s * pstep + prow0) * 2]);
+    for (int s = 0; s < n_splits; ++s) {
+      const int64_t prow = s * pstep + prow0;
+      const float2 ml = *reinterpret_cast<const float2 *>(a.ws + sp.ml_off + prow * 2);
+      const float w = (ml.x == -INFINITY) ? 0.f : fast_exp2(ml.x - mmax);
+      lsum += w * ml.y;
+      const float4 ov = *reinterpret_cast<const float4 *>(a.ws + sp.ws_off + prow * D + 4 * d4);
+      acc.x += w * ov.x;
+      acc.y += w * ov.y;
+      acc.z += w * ov.z;
+      acc.w += w * ov.w;
+    }
   }
   const float inv = 1.0f / lsum;
   uint16_t *orow = a.out + ((int64_t)(sp.q_start + row) * a.n_q_heads + head) * D + 4 * d4;
