@@ -35,6 +35,7 @@ METRIC = "suffix-redecode attn TFLOP/s + re-phase/splice GB/s, % of MI355X roofl
 # Measured HBM traffic of one attention call (rocprofv3 FETCH_SIZE / WRITE_SIZE, scaled by a
 # plain copy), valid only for the kernel sources it was taken on.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_attn_cfg3_qwen14b.txt")
+MFMA_FILE = os.path.join(ROOT, "profiles", "mfma_util_attn_cfg3_qwen14b.txt")
 ATTN_SOURCES = ["attn_bf16_dma.hip", "attn_bf16.hip", "attn_common.h", "device_common.h",
                 "launch.h"]
 
@@ -47,21 +48,42 @@ def attn_sources_sha() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(cfg: int):
-    """Bytes per attention call from the committed counter summary, or None when it was taken
-    on other kernel sources or another workload."""
+def counter_summary(path: str, cfg: int):
+    """Key/value lines of a committed counter summary, or None when it was taken on other
+    attention kernel sources or another workload."""
     try:
         kv = {}
-        with open(TRAFFIC_FILE) as fh:
+        with open(path) as fh:
             for line in fh:
                 if line.startswith("#") or ":" not in line:
                     continue
                 k, v = line.split(":", 1)
                 kv[k.strip()] = v.strip()
-        if kv.get("workload") != f"cfg{cfg}" or kv.get("kernel_sources_sha256") != attn_sources_sha():
-            return None
-        return int(kv["traffic_bytes_per_launch"])
-    except (OSError, KeyError, ValueError):
+    except OSError:
+        return None
+    if kv.get("workload") != f"cfg{cfg}" or kv.get("kernel_sources_sha256") != attn_sources_sha():
+        return None
+    return kv
+
+
+def measured_traffic(cfg: int):
+    """Bytes per attention call (FETCH_SIZE + WRITE_SIZE, copy-scaled) from the committed
+    counter summary, or None."""
+    kv = counter_summary(TRAFFIC_FILE, cfg)
+    try:
+        return int(kv["traffic_bytes_per_launch"]) if kv else None
+    except (KeyError, ValueError):
+        return None
+
+
+def measured_mfma_busy(cfg: int):
+    """Fraction of SIMD cycles with the MFMA pipe busy in the attention kernel
+    (SQ_VALU_MFMA_BUSY_CYCLES over GRBM_GUI_ACTIVE x SIMDs) from the committed counter
+    summary, or None."""
+    kv = counter_summary(MFMA_FILE, cfg)
+    try:
+        return float(kv["mfma_busy_frac"]) if kv else None
+    except (KeyError, ValueError):
         return None
 
 
@@ -636,6 +658,9 @@ def main():
             "frac": attn_tflops / MFMA_BF16_PEAK_TFLOPS,
             "traffic": measured_traffic(wl.cfg),
             "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-scaled)",
+            "mfma_busy": measured_mfma_busy(wl.cfg),
+            "mfma_busy_unit": ("fraction of SIMD cycles with the MFMA pipe busy, attention kernel "
+                               "(SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs))"),
             "algorithmic_flops_per_launch": fl_layer,
             "mean_launch_ms": mean["attn"],
         },
