@@ -92,6 +92,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
   constexpr int ROWB = D * 2;                 // bytes per K or V row
   constexpr int TILEB = KT * ROWB;            // bytes per K or V tile
   constexpr float kSlack = 8.0f;              // lazy rescale: p <= 2^8 between rescales
+  constexpr int kPrioPV = 2;                  // wave priority of the PV phase
   __shared__ __align__(1024) char smem[2 * 2 * TILEB];   // K buffers 0, 1, V buffers 0, 1
   __shared__ __align__(16) int32_t pg[kMaxSplitKeys / kPage + 8];
 
@@ -229,58 +230,110 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
       }
   };
 
+  // S(t) needs the causal / tail mask when its tile crosses this wave's diagonal or the split end
+  auto needs_mask = [&](int t) {
+    const int kt = k_begin + t * KT;
+    return (kt + KT > k_end) || (kt + KT - 1 > qpos0);
+  };
+  // soft cap of S(t)
+  auto cap = [&](f32x16 *sc) {
+    if constexpr (CAP) {
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sc[kb][v] = a.cap_out * tanh_fast(sc[kb][v] * a.cap_in);
+    }
+  };
+  // causal / tail mask of S(t) (tiles for which needs_mask(t))
+  auto mask = [&](f32x16 *sc, int t) {
+    const int lim = min(qpos0 + j, k_end - 1) - (k_begin + t * KT) - 4 * hh;
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        if (32 * kb + 8 * (v >> 2) + (v & 3) > lim) sc[kb][v] = -INFINITY;
+  };
+  // row maximum of S(t) in log2 units
+  auto row_max = [&](const f32x16 *sc) -> float {
+    float mt = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sc[kb][v]);
+    return max_halves(mt) * c_scale;
+  };
+  // P of the 32 keys of score block kb, as the B operands of two 16-key PV steps; adds their
+  // sum to l
+  auto softmax_block = [&](const f32x16 &sc, float nm, bf16x8 *pb) {
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p0 = fast_exp2(fmaf(sc[8 * hf + 2 * e], c_scale, nm));
+        const float p1 = fast_exp2(fmaf(sc[8 * hf + 2 * e + 1], c_scale, nm));
+        w[e] = pack_bf16x2(p0, p1);
+        l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), ones, l, false);
+      }
+      pb[hf] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
+    }
+  };
+  // O^T += V^T P^T over the 16 keys of step ks of the V tile at vl
+  auto pv_step = [&](const char *vl, int ks, const bf16x8 &pbv) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const char *p = vl + ks * 16 * ROWB + offv[db];
+      const bf16x8 va = tr_read_pair(p, p + 8 * ROWB);
+      o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pbv, o[db], 0, 0, 0);
+    }
+  };
+
   // Pipeline, per iteration t: the DMA of K[t + 2] and V[t + 1] runs while the wave computes
-  // S(t + 1) = K[t + 1] Q^T on the MFMA pipe, the softmax of S(t) on the VALU, and
-  // O += V[t] P(t).  K[t + 1] and V[t] are resident: K buffers hold tiles t + 1 and t + 2,
-  // V buffers tiles t and t + 1.  Pages: pk = page of tile t + 2 (K DMA), pv = of tile t + 1.
+  // S(t + 1) = K[t + 1] Q^T and O += V[t] P(t).  K buffers hold tiles t + 1 and t + 2, V
+  // buffers tiles t and t + 1.  Pages: pk = page of tile t + 2 (K DMA), pgv = of tile t + 1.
+  // Within the wave the matrix and vector work alternate: the S(t + 1) MFMAs run beside the
+  // exponentials of S(t)'s first 32 keys, the PV MFMAs of those keys beside the exponentials of
+  // the other 32, and the last PV MFMAs beside the soft cap and maximum of S(t + 1), which the
+  // next iteration's rescale needs.  The region has no branch, so the compiler's schedule can
+  // follow the MFMA / LDS read / VALU pattern set below; the causal and tail masks, needed on
+  // few tiles, are applied at the top of the next iteration.
   f32x16 sa[NKB], sb[NKB];
-  uint32_t pv = 0, pk = 0;
+  uint32_t pgv = 0, pk = 0;
   if (n_tiles > 0) {
     const uint32_t p0 = full(0) ? page_of(0) : 0;
     dma_tile(0, 0, kbuf(0), p0);
     dma_tile(0, 1, vbuf(0), p0);
     if (n_tiles > 1) {
-      pv = full(1) ? page_of(1) : 0;
-      dma_tile(1, 0, kbuf(1), pv);
+      pgv = full(1) ? page_of(1) : 0;
+      dma_tile(1, 0, kbuf(1), pgv);
     }
     if (n_tiles > 2 && full(2)) pk = page_of(2);
   }
   wait_vm<0>();
   tile_barrier();
-  if (active && n_tiles > 0) qk(kbuf(0), sa);
+  float mt_cur = -INFINITY;                     // row maximum of S(t), log2 units
+  if (active && n_tiles > 0) {
+    qk(kbuf(0), sa);
+    cap(sa);
+    mt_cur = row_max(sa);        // unmasked: step 0 masks S(0) and takes its maximum again
+  }
   tile_barrier();    // K buffer 0 is refilled in iteration 0
 
-  auto step = [&](int t, auto parity, f32x16 *s_cur, f32x16 *s_nxt) {
+  // NX: whether tile t + 1 exists (the last tile is peeled off the loop)
+  auto step = [&](int t, auto parity, f32x16 *s_cur, f32x16 *s_nxt, auto next) {
     constexpr int P = decltype(parity)::value;     // t & 1
-    const int kt = k_begin + t * KT;
+    constexpr bool NX = decltype(next)::value;
     if (t + 2 < n_tiles) dma_tile(t + 2, 0, kbuf(P), pk);
-    if (t + 1 < n_tiles) dma_tile(t + 1, 1, vbuf(P ^ 1), pv);
+    if (t + 1 < n_tiles) dma_tile(t + 1, 1, vbuf(P ^ 1), pgv);
     if (active) {
-      if constexpr (CAP) {
-#pragma unroll
-        for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) s_cur[kb][v] = a.cap_out * tanh_fast(s_cur[kb][v] * a.cap_in);
+      // the maximum of S(t) was taken before its mask: on the few tiles that need one, mask
+      // and take it again
+      if (needs_mask(t)) {
+        mask(s_cur, t);
+        mt_cur = row_max(s_cur);
       }
-      // causal / tail mask of S(t), on tiles that cross this wave's diagonal or the split end
-      if ((kt + KT > k_end) || (kt + KT - 1 > qpos0)) {
-        const int lim = min(qpos0 + j, k_end - 1) - kt - 4 * hh;
-#pragma unroll
-        for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-          for (int v = 0; v < 16; ++v)
-            if (32 * kb + 8 * (v >> 2) + (v & 3) > lim) s_cur[kb][v] = -INFINITY;
-      }
-      // S(t + 1) on the MFMA pipe, interleaved with the max of S(t)
-      if (t + 1 < n_tiles) qk(kbuf(P ^ 1), s_nxt);
-      float mt = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) mt = fmaxf(mt, s_cur[kb][v]);
-      mt = max_halves(mt) * c_scale;
-      if (__builtin_amdgcn_ballot_w64(mt > m_ref + kSlack) != 0) {
-        const float m_new = fmaxf(m_ref, mt);
+      if (__builtin_amdgcn_ballot_w64(mt_cur > m_ref + kSlack) != 0) {
+        const float m_new = fmaxf(m_ref, mt_cur);
         const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(m_ref - m_new);
         l *= alpha;
 #pragma unroll
@@ -291,44 +344,65 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
       }
       const float nm = (m_ref == -INFINITY) ? 0.f : -m_ref;
       const char *vl = vbuf(P);
-      // The softmax of S(t) and O += V P run at a raised wave priority: of the two waves that
-      // share a SIMD, the one in this phase issues first, so its exponentials and PV MFMAs
-      // interleave with the other wave's S^T MFMAs instead of queueing behind them (measured
-      // about 4% faster per call at config 3; results are bit-identical).
-      __builtin_amdgcn_s_setprio(2);
+      bf16x8 pb[4];
+      if constexpr (NX) qk(kbuf(P ^ 1), s_nxt);
+      softmax_block(s_cur[0], nm, pb);
+      if constexpr (NX) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
-      for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          uint32_t w[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float p0 = fast_exp2(fmaf(s_cur[kb][8 * hf + 2 * e], c_scale, nm));
-            const float p1 = fast_exp2(fmaf(s_cur[kb][8 * hf + 2 * e + 1], c_scale, nm));
-            w[e] = pack_bf16x2(p0, p1);
-            l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), ones, l, false);
-          }
-          const bf16x8 pbv = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
-          const int ks = 2 * kb + hf;
-#pragma unroll
-          for (int db = 0; db < NDB; ++db) {
-            const char *p = vl + ks * 16 * ROWB + offv[db];
-            const bf16x8 va = tr_read_pair(p, p + 8 * ROWB);
-            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pbv, o[db], 0, 0, 0);
-          }
+        for (int i = 0; i < 16; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
         }
+      }
+      // O += V P and what follows run at a raised wave priority: of the two waves that share a
+      // SIMD, the one in this phase issues first
+      __builtin_amdgcn_s_setprio(kPrioPV);
+      pv_step(vl, 0, pb[0]);
+      pv_step(vl, 1, pb[1]);
+      softmax_block(s_cur[1], nm, pb + 2);
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 1);
+      }
+      pv_step(vl, 2, pb[2]);
+      pv_step(vl, 3, pb[3]);
+      if constexpr (NX) {
+        cap(s_nxt);
+        mt_cur = row_max(s_nxt);
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 2);
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 2);
+      }
     }
     __builtin_amdgcn_s_setprio(0);
     // pages for the next iteration's DMA (the LDS read overlaps the wait below)
-    pv = pk;
+    pgv = pk;
     if (t + 3 < n_tiles && full(t + 3)) pk = page_of(t + 3);
     // K[t + 2] and V[t + 1], issued above, are read in the next iteration
     wait_vm<0>();
     tile_barrier();
   };
-  for (int t = 0; t < n_tiles; t += 2) {
-    step(t, std::integral_constant<int, 0>{}, sa, sb);
-    if (t + 1 < n_tiles) step(t + 1, std::integral_constant<int, 1>{}, sb, sa);
+  using P0 = std::integral_constant<int, 0>;
+  using P1 = std::integral_constant<int, 1>;
+  int t = 0;
+  for (; t + 2 < n_tiles; t += 2) {
+    step(t, P0{}, sa, sb, std::true_type{});
+    step(t + 1, P1{}, sb, sa, std::true_type{});
+  }
+  // the last one or two tiles
+  if (t + 1 < n_tiles) {
+    step(t, P0{}, sa, sb, std::true_type{});
+    step(t + 1, P1{}, sb, sa, std::false_type{});
+  } else if (t < n_tiles) {
+    step(t, P0{}, sa, sb, std::false_type{});
   }
 
   // ---- epilogue
