@@ -319,10 +319,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
   }
   tile_barrier();    // K buffer 0 is refilled in iteration 0
 
-  // NX: whether tile t + 1 exists (the last tile is peeled off the loop)
-  auto step = [&](int t, auto parity, f32x16 *s_cur, f32x16 *s_nxt, auto next) {
+  auto step = [&](int t, auto parity, f32x16 *s_cur, f32x16 *s_nxt) {
     constexpr int P = decltype(parity)::value;     // t & 1
-    constexpr bool NX = decltype(next)::value;
     if (t + 2 < n_tiles) dma_tile(t + 2, 0, kbuf(P), pk);
     if (t + 1 < n_tiles) dma_tile(t + 1, 1, vbuf(P ^ 1), pgv);
     if (active) {
@@ -345,16 +343,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
       const float nm = (m_ref == -INFINITY) ? 0.f : -m_ref;
       const char *vl = vbuf(P);
       bf16x8 pb[4];
-      if constexpr (NX) qk(kbuf(P ^ 1), s_nxt);
+      qk(kbuf(P ^ 1), s_nxt);
       softmax_block(s_cur[0], nm, pb);
-      if constexpr (NX) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
-        }
+      for (int i = 0; i < 16; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
       }
       // O += V P and what follows run at a raised wave priority: of the two waves that share a
       // SIMD, the one in this phase issues first
@@ -371,10 +367,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
       }
       pv_step(vl, 2, pb[2]);
       pv_step(vl, 3, pb[3]);
-      if constexpr (NX) {
-        cap(s_nxt);
-        mt_cur = row_max(s_nxt);
-      }
+      cap(s_nxt);
+      mt_cur = row_max(s_nxt);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
@@ -390,19 +384,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
     wait_vm<0>();
     tile_barrier();
   };
-  using P0 = std::integral_constant<int, 0>;
-  using P1 = std::integral_constant<int, 1>;
-  int t = 0;
-  for (; t + 2 < n_tiles; t += 2) {
-    step(t, P0{}, sa, sb, std::true_type{});
-    step(t + 1, P1{}, sb, sa, std::true_type{});
-  }
-  // the last one or two tiles
-  if (t + 1 < n_tiles) {
-    step(t, P0{}, sa, sb, std::true_type{});
-    step(t + 1, P1{}, sb, sa, std::false_type{});
-  } else if (t < n_tiles) {
-    step(t, P0{}, sa, sb, std::false_type{});
+  // Every iteration computes S(t + 1): on the last tile from a K buffer whose contents are
+  // stale, a result never used.  A branch there would split the scheduled region, and peeling
+  // the last tile off the loop made the register allocator spill.
+  for (int t = 0; t < n_tiles; t += 2) {
+    step(t, std::integral_constant<int, 0>{}, sa, sb);
+    if (t + 1 < n_tiles) step(t + 1, std::integral_constant<int, 1>{}, sb, sa);
   }
 
   // ---- epilogue
