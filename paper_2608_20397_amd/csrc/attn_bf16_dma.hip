@@ -262,8 +262,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
       for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sc[kb][v]);
     return max_halves(mt) * c_scale;
   };
-  // P of the 32 keys of score block kb, as the B operands of two 16-key PV steps; adds their
-  // sum to l
+  // P of the 32 keys of a score block, as the B operands of two 16-key PV steps; adds their
+  // sum to l (softmax_half: one of the two 16-key halves)
   auto softmax_block = [&](const f32x16 &sc, float nm, bf16x8 *pb) {
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
@@ -277,6 +277,17 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
       }
       pb[hf] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
     }
+  };
+  auto softmax_half = [&](const f32x16 &sc, int hf, float nm, bf16x8 &pbo) {
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float p0 = fast_exp2(fmaf(sc[8 * hf + 2 * e], c_scale, nm));
+      const float p1 = fast_exp2(fmaf(sc[8 * hf + 2 * e + 1], c_scale, nm));
+      w[e] = pack_bf16x2(p0, p1);
+      l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), ones, l, false);
+    }
+    pbo = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
   };
   // O^T += V^T P^T over the 16 keys of step ks of the V tile at vl
   auto pv_step = [&](const char *vl, int ks, const bf16x8 &pbv) {
@@ -292,9 +303,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
   // S(t + 1) = K[t + 1] Q^T and O += V[t] P(t).  K buffers hold tiles t + 1 and t + 2, V
   // buffers tiles t and t + 1.  Pages: pk = page of tile t + 2 (K DMA), pgv = of tile t + 1.
   // Within the wave the matrix and vector work alternate: the S(t + 1) MFMAs run beside the
-  // exponentials of S(t)'s first 32 keys, the PV MFMAs of those keys beside the exponentials of
-  // the other 32, and the last PV MFMAs beside the soft cap and maximum of S(t + 1), which the
-  // next iteration's rescale needs.  The region has no branch, so the compiler's schedule can
+  // exponentials of S(t)'s first 48 keys, the PV MFMAs beside the exponentials of the last 16
+  // and the soft cap and maximum of S(t + 1), which the next iteration's rescale needs.  The region has no branch, so the compiler's schedule can
   // follow the MFMA / LDS read / VALU pattern set below; the causal and tail masks, needed on
   // few tiles, are applied at the top of the next iteration.
   f32x16 sa[NKB], sb[NKB];
@@ -345,35 +355,36 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_d128_dma_kernel(const AttnAr
       bf16x8 pb[4];
       qk(kbuf(P ^ 1), s_nxt);
       softmax_block(s_cur[0], nm, pb);
+      softmax_half(s_cur[1], 0, nm, pb[2]);
       __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
       }
       // O += V P and what follows run at a raised wave priority: of the two waves that share a
       // SIMD, the one in this phase issues first
       __builtin_amdgcn_s_setprio(kPrioPV);
       pv_step(vl, 0, pb[0]);
       pv_step(vl, 1, pb[1]);
-      softmax_block(s_cur[1], nm, pb + 2);
+      pv_step(vl, 2, pb[2]);
+      softmax_half(s_cur[1], 1, nm, pb[3]);
       __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < 12; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
         __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
-        __builtin_amdgcn_sched_group_barrier(0x002, 6, 1);
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 1);
       }
-      pv_step(vl, 2, pb[2]);
       pv_step(vl, 3, pb[3]);
       cap(s_nxt);
       mt_cur = row_max(s_nxt);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < 4; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
         __builtin_amdgcn_sched_group_barrier(0x100, 2, 2);
-        __builtin_amdgcn_sched_group_barrier(0x002, 2, 2);
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 2);
       }
     }
     __builtin_amdgcn_s_setprio(0);
