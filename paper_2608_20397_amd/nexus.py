@@ -10,7 +10,7 @@ from __future__ import annotations
 
 import ctypes as C
 import os
-from dataclasses import dataclass
+from dataclasses import dataclass, field
 
 import torch
 
@@ -122,6 +122,23 @@ def _ptr(t):
     return C.c_void_p(t.data_ptr()) if t is not None else C.c_void_p(0)
 
 
+def _on_device(*named):
+    """Every given (name, tensor) pair must be a device tensor, all on one device; returns that
+    device.  The kernels dereference every pointer they get as a device address, so a host
+    tensor must never reach them."""
+    dev = None
+    for name, t in named:
+        if t is None:
+            continue
+        if not isinstance(t, torch.Tensor) or not t.is_cuda:
+            raise NexusError(EINVAL, f"{name} must be a device tensor")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise NexusError(EINVAL, f"{name} is on {t.device}, the other operands on {dev}")
+    return dev
+
+
 @dataclass
 class Block:
     """A compiled KV block in HBM: k, v [n_layers][n_tokens][n_kv_heads][head_dim]."""
@@ -135,6 +152,7 @@ class Block:
         L, T, H, D = self.k.shape
         if tuple(self.v.shape) != (L, T, H, D) or not (self.k.is_contiguous() and self.v.is_contiguous()):
             raise NexusError(ESHAPE, "block k/v must be contiguous [L][T][H][D] of equal shape")
+        _on_device(("block k", self.k), ("block v", self.v))
         return CBlock(self.k.data_ptr(), self.v.data_ptr(), L, T, H, D, _dtype_code(self.k),
                       self.rope_style, self.base_pos, self.rope_base)
 
@@ -142,18 +160,25 @@ class Block:
 @dataclass
 class PagedKVCache:
     """k [L][n_phys_pages][H][16][D]; v the same or, transposed, [L][H][D][n_phys_pages*16];
-    page_map int32 [n_logical_pages] on the device."""
+    page_map int32 [n_logical_pages] on the device.
+
+    The kernels read the page map's entries on the device without a host check, so the map is
+    validated here (``nexus_check_page_table`` on a host copy: every entry a distinct physical
+    page) the first time a call uses it and again whenever it has changed since (another tensor,
+    or an in-place write that bumped its version counter)."""
     k: torch.Tensor
     v: torch.Tensor
     page_map: torch.Tensor
     rope_base: float
     v_layout: int = V_ROWMAJOR
     rope_style: int = ROPE_NEOX
+    _map_checked: tuple | None = field(default=None, init=False, repr=False, compare=False)
 
     def c(self) -> CKvCache:
         L, npp, H, P, D = self.k.shape
         if P != PAGE or not (self.k.is_contiguous() and self.v.is_contiguous()):
             raise NexusError(ESHAPE, "cache k must be contiguous [L][pages][H][16][D]")
+        _on_device(("cache k", self.k), ("cache v", self.v), ("page_map", self.page_map))
         want_v = (L, H, D, npp * P) if self.v_layout == V_TRANSPOSED else (L, npp, H, P, D)
         if tuple(self.v.shape) != want_v:
             raise NexusError(ESHAPE, f"cache v must be {want_v}, got {tuple(self.v.shape)}")
@@ -163,9 +188,16 @@ class PagedKVCache:
                         _dtype_code(self.k), self.v_layout, self.rope_style, self.rope_base)
 
     def pt(self) -> CPageTable:
-        if self.page_map.dtype != torch.int32 or not self.page_map.is_contiguous():
-            raise NexusError(EINVAL, "page_map must be contiguous int32")
-        return CPageTable(self.page_map.data_ptr(), self.page_map.numel())
+        pm = self.page_map
+        if pm.dtype != torch.int32 or pm.dim() != 1 or not pm.is_contiguous():
+            raise NexusError(EINVAL, "page_map must be a contiguous int32 vector")
+        _on_device(("cache k", self.k), ("page_map", pm))
+        npp = self.k.shape[1]
+        key = (pm.data_ptr(), pm._version, pm.numel(), npp)
+        if self._map_checked != key:
+            check_page_table(pm.cpu().numpy(), npp)      # raises NexusError(ERANGE)
+            self._map_checked = key
+        return CPageTable(pm.data_ptr(), pm.numel())
 
     @property
     def n_layers(self):
@@ -174,6 +206,7 @@ class PagedKVCache:
 
 def splice_pages(cache: PagedKVCache, block: Block, offset: int):
     cc, pt, cb = cache.c(), cache.pt(), block.c()
+    _on_device(("cache k", cache.k), ("block k", block.k))
     _check(lib().nexus_splice_pages(C.byref(cc), C.byref(pt), C.byref(cb), offset, _stream()),
            "nexus_splice_pages")
 
@@ -182,6 +215,7 @@ def splice_rephase_pages(cache: PagedKVCache, block: Block, offset: int, dst_pos
     """Splice ``block`` at ``offset`` with its keys re-anchored from block.base_pos to
     ``dst_pos`` in the same pass (the block itself is left as it is)."""
     cc, pt, cb = cache.c(), cache.pt(), block.c()
+    _on_device(("cache k", cache.k), ("block k", block.k))
     _check(lib().nexus_splice_rephase_pages(C.byref(cc), C.byref(pt), C.byref(cb), offset, dst_pos,
                                             _stream()), "nexus_splice_rephase_pages")
 
@@ -193,6 +227,7 @@ def rope_append(cache: PagedKVCache, k: torch.Tensor, v: torch.Tensor, offset: i
     L, T, H, D = k.shape
     if tuple(v.shape) != (L, T, H, D) or not (k.is_contiguous() and v.is_contiguous()):
         raise NexusError(ESHAPE, "k/v must be contiguous [L][T][H][D] of equal shape")
+    _on_device(("cache k", cache.k), ("k", k), ("v", v))
     if (L, H, D) != (cc.n_layers, cc.n_kv_heads, cc.head_dim) or _dtype_code(k) != cc.dtype \
             or _dtype_code(v) != cc.dtype:
         raise NexusError(ESHAPE, "k/v must match the cache's layers, heads, head_dim and dtype")
@@ -244,6 +279,7 @@ def suffix_attn(q: torch.Tensor, cache: PagedKVCache, layer: int, n_past: int,
     elif out.shape != q.shape or out.dtype != q.dtype or not out.is_contiguous():
         raise NexusError(EINVAL, "out must be contiguous, shaped and typed like q")
     cc, pt = cache.c(), cache.pt()
+    _on_device(("cache k", cache.k), ("q", q), ("out", out), ("workspace", workspace))
     ws_bytes = lib().nexus_suffix_attn_workspace(n_s, hq, C.byref(cc), n_past)
     if ws_bytes == (1 << 64) - 1:
         raise NexusError(EINVAL, "nexus_suffix_attn_workspace")
@@ -269,9 +305,14 @@ def suffix_attn_varlen(q: torch.Tensor, q_start, seq_len, seq_n_past, cache: Pag
     _, hq, _ = q.shape
     if not q.is_contiguous():
         raise NexusError(EINVAL, "q must be contiguous")
+    if q.dtype != cache.k.dtype:
+        raise NexusError(EDTYPE, "q dtype differs from the cache")
     if out is None:
         out = torch.empty_like(q)
+    elif out.shape != q.shape or out.dtype != q.dtype or not out.is_contiguous():
+        raise NexusError(EINVAL, "out must be contiguous, shaped and typed like q")
     cc, pt = cache.c(), cache.pt()
+    _on_device(("cache k", cache.k), ("q", q), ("out", out), ("workspace", workspace))
     ws_bytes = lib().nexus_suffix_attn_varlen_workspace(n, qs, ls, ps, hq, C.byref(cc))
     if ws_bytes == (1 << 64) - 1:
         raise NexusError(EINVAL, "nexus_suffix_attn_varlen_workspace")
@@ -317,6 +358,8 @@ def decode_attn(q: torch.Tensor, cache: PagedKVCache, maps: torch.Tensor, seq_le
     elif out.shape != q.shape or out.dtype != q.dtype or not out.is_contiguous():
         raise NexusError(EINVAL, "out must be contiguous, shaped and typed like q")
     cc = cache.c()
+    _on_device(("cache k", cache.k), ("q", q), ("maps", maps), ("seq_len", seq_len),
+               ("out", out), ("workspace", workspace))
     ws_bytes = lib().nexus_decode_attn_workspace(n, hq, C.byref(cc), max_seq_len)
     if ws_bytes == (1 << 64) - 1:
         raise NexusError(EINVAL, "nexus_decode_attn_workspace")
@@ -343,6 +386,7 @@ def kv_copy_tokens(cache: PagedKVCache, src_map: torch.Tensor, dst_map: torch.Te
     if src_map.numel() != dst_map.numel():
         raise NexusError(EINVAL, "maps differ in length")
     cc = cache.c()
+    _on_device(("cache k", cache.k), ("src_map", src_map), ("dst_map", dst_map))
     _check(lib().nexus_kv_copy_tokens(C.byref(cc), _map_arg(src_map, "src_map"),
                                       _map_arg(dst_map, "dst_map"), src_map.numel(), t0,
                                       n_tokens, _stream()), "nexus_kv_copy_tokens")
@@ -355,6 +399,7 @@ def kv_share_prefix(cache: PagedKVCache, src_map: torch.Tensor, dst_map: torch.T
     if src_map.numel() != dst_map.numel():
         raise NexusError(EINVAL, "maps differ in length")
     cc = cache.c()
+    _on_device(("cache k", cache.k), ("src_map", src_map), ("dst_map", dst_map))
     _check(lib().nexus_kv_share_prefix(C.byref(cc), _map_arg(src_map, "src_map"),
                                        _map_arg(dst_map, "dst_map"), src_map.numel(), n_tokens,
                                        _stream()), "nexus_kv_share_prefix")
@@ -393,6 +438,7 @@ def slb_quantize(x: torch.Tensor, out=None):
         if (q.dtype != torch.int8 or tuple(q.shape) != (n, dim) or not q.is_contiguous()
                 or s.dtype != torch.float32 or s.numel() != n):
             raise NexusError(EINVAL, "out must be (int8 [n][dim], fp32 [n]) contiguous tensors")
+    _on_device(("x", x), ("codes", q), ("scales", s))
     _check(lib().nexus_slb_quantize(_ptr(x), n, dim, _ptr(q), _ptr(s), _stream()),
            "nexus_slb_quantize")
     return q, s
@@ -411,7 +457,10 @@ def slb_scan(tools: torch.Tensor, tool_scale: torch.Tensor, queries: torch.Tenso
     n_q = queries.shape[0]
     if queries.shape[1] != dim or tool_scale.numel() != n_tools or query_scale.numel() != n_q:
         raise NexusError(ESHAPE, "slb_scan: operand shapes disagree")
-    dev = tools.device
+    dev = _on_device(("tools", tools), ("tool_scale", tool_scale), ("queries", queries),
+                     ("query_scale", query_scale), ("workspace", workspace))
+    if out is not None:
+        _on_device(("tools", tools), *[(f"out[{i}]", t) for i, t in enumerate(out)])
     if out is None:
         out = (torch.empty((n_q, k), dtype=torch.int32, device=dev),
                torch.empty((n_q, k), dtype=torch.float32, device=dev),

@@ -355,3 +355,24 @@ def test_slb_validation_fails_closed():
     assert L.nexus_slb_scan_workspace(250, 1, 768, 2) == 0          # one range: no workspace
     assert L.nexus_slb_quantize(None, 1, 64, o1, o2, s) == N.EINVAL
     assert L.nexus_slb_quantize(t, 0, 64, o1, o2, s) == N.EINVAL
+
+
+def test_binding_rejects_host_tensors():
+    """Every tensor the binding hands to the library must live on the device: host tensors are
+    refused with EINVAL before any call (no GPU is needed to check this)."""
+    import torch
+    k = torch.zeros(1, 2, 1, 16, 64, dtype=torch.bfloat16)
+    cache = N.PagedKVCache(k, k.clone(), torch.arange(2, dtype=torch.int32), 1e4)
+    with pytest.raises(N.NexusError) as e:
+        cache.c()
+    assert e.value.status == N.EINVAL
+    with pytest.raises(N.NexusError) as e:
+        cache.pt()
+    assert e.value.status == N.EINVAL
+    b = torch.zeros(1, 4, 1, 64, dtype=torch.bfloat16)
+    with pytest.raises(N.NexusError) as e:
+        N.Block(b, b.clone(), 0, 1e4).c()
+    assert e.value.status == N.EINVAL
+    with pytest.raises(N.NexusError) as e:
+        N.slb_quantize(torch.zeros(2, 64))
+    assert e.value.status == N.EINVAL

@@ -20,23 +20,9 @@ from paper_2608_20397_amd import nexus as N
 from synth import PAGE
 from synth import gen as G
 
-from _pipeline import VL, check_keys, gpu_build_cache, oracle_cache, range_mask
+from _pipeline import VL, check_keys, close_keys, gpu_build_cache, oracle_cache, range_mask
 
 pytestmark = pytest.mark.gpu
-
-
-def _close_keys(got_bits, want_bits, dtype, tag):
-    if dtype == "bf16":
-        a = O.bf16_bits_to_f64(got_bits)
-        b = O.bf16_bits_to_f64(want_bits)
-        ulp = np.maximum(np.abs(b) * 2.0 ** -7, 2.0 ** -133)
-        assert np.all(np.abs(a - b) <= ulp + 1e-300), f"{tag}: more than 1 ulp"
-        exact = np.mean(got_bits == want_bits)
-        assert exact >= 0.999, f"{tag}: only {exact:.5f} exactly rounded"
-    else:
-        a = got_bits.view(np.float32).astype(np.float64)
-        b = want_bits.view(np.float32).astype(np.float64)
-        assert np.max(np.abs(a - b)) <= 1e-5, f"{tag}: f32 keys off by {np.max(np.abs(a - b))}"
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 4, 5])
@@ -126,7 +112,7 @@ def test_rope_append_matches_oracle_rope(dtype, style, D, v_layout, base, offset
     for t in range(offset, offset + T):
         untouched[:, pm[t // PAGE], :, t % PAGE, :] = False
     assert np.array_equal(gk[untouched], ok[untouched]), "keys written outside the slots"
-    _close_keys(gk[~untouched], ok[~untouched], dtype, f"{dtype} {style} D{D}")
+    close_keys(gk[~untouched], ok[~untouched], dtype, f"{dtype} {style} D{D}")
     assert np.array_equal(G.torch_to_bits(k_dev), k_bits)          # inputs are not modified
 
 
@@ -149,4 +135,4 @@ def test_rope_append_keys_at_their_positions():
     lk, _ = O.gather_logical(G.torch_to_bits(a.k), G.torch_to_bits(a.v), pm, 112, PAGE)
     want = np.stack([O.round_to_storage(O.rope(O.storage_to_f64(pre_bits[l], "bf16"),
                                                64 + np.arange(T), base), "bf16") for l in range(L)])
-    _close_keys(lk[:, 64:112], want, "bf16", "append at 64")
+    close_keys(lk[:, 64:112], want, "bf16", "append at 64")

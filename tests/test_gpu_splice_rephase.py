@@ -137,3 +137,40 @@ def test_splice_rejects_mismatched_header():
     assert e.value.status == N.EROPE
     torch.cuda.synchronize()
     assert np.array_equal(G.torch_to_bits(cache.k), before)
+
+
+def test_bad_page_map_is_rejected_before_launch():
+    """The binding validates the page map (host copy, every entry a distinct physical page) on
+    first use and after every in-place change: a duplicated or out-of-range entry is refused with
+    ERANGE before any kernel runs, and the cache keeps its bits."""
+    wl = G.get_workload(2)
+    kb, vb = G.empty_cache_bits(wl, 1)
+    npp = wl.n_pages
+    pm = torch.arange(npp, dtype=torch.int32, device="cuda")
+    cache = N.PagedKVCache(G.bits_to_torch(kb, "bf16", "cuda"), G.bits_to_torch(vb, "bf16", "cuda"),
+                           pm, 1e6)
+    z = torch.zeros(1, 16, 8, 128, dtype=torch.bfloat16, device="cuda")
+    blk = N.Block(z, z.clone(), 0, 1e6)
+    N.splice_pages(cache, blk, 0)                  # valid map
+    torch.cuda.synchronize()
+    before_k, before_v = G.torch_to_bits(cache.k), G.torch_to_bits(cache.v)
+    pm[3] = pm[4]                                  # duplicate entry (in-place write)
+    with pytest.raises(N.NexusError) as e:
+        N.splice_pages(cache, N.Block(z + 1, z + 1, 0, 1e6), 0)
+    assert e.value.status == N.ERANGE
+    pm[3] = npp                                    # out of range
+    with pytest.raises(N.NexusError) as e:
+        N.rephase_k_paged(cache, 0, 16, 0, 5, 1e6)
+    assert e.value.status == N.ERANGE
+    q = torch.zeros(4, 40, 128, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(N.NexusError) as e:
+        N.suffix_attn(q, cache, 0, 0)
+    assert e.value.status == N.ERANGE
+    torch.cuda.synchronize()
+    assert np.array_equal(G.torch_to_bits(cache.k), before_k)
+    assert np.array_equal(G.torch_to_bits(cache.v), before_v)
+    pm[3] = 3                                      # repaired: accepted again
+    N.splice_pages(cache, blk, 0)
+    with pytest.raises(N.NexusError) as e:         # a host page map never reaches a kernel
+        N.splice_pages(N.PagedKVCache(cache.k, cache.v, pm.cpu(), 1e6), blk, 0)
+    assert e.value.status == N.EINVAL
