@@ -202,6 +202,30 @@ size_t nexus_suffix_attn_workspace(int32_t n_s, int32_t n_q_heads, const nexus_k
                                    int64_t n_past);
 
 /*
+ * nexus_suffix_attn for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same computation with no
+ * workspace argument.  The split-K partials live in a static device array of
+ * NEXUS_NOALLOC_SCRATCH_BYTES that each GPU the library runs on holds until the process ends.
+ * The call allocates no device memory (its host-side plan uses a few small host buffers).
+ *   - Plan: the key split of least estimated time among those whose partials fit the array;
+ *     whenever the plan of nexus_suffix_attn fits (its workspace size <= the array), it is that
+ *     plan and the output is bit-identical to nexus_suffix_attn's.
+ *   - Limit: when no split fits (a suffix too long for the array), NEXUS_EWORKSPACE and nothing
+ *     is enqueued.
+ *   - Device: the array of the calling thread's current device is used; a non-null `stream`
+ *     must belong to that device (else NEXUS_EINVAL).
+ *   - Concurrency: every call on one GPU shares that GPU's array, which keeps the last call's
+ *     contents (nothing in it needs to start at zero).  Calls that overlap on one GPU (other
+ *     streams, other host threads) race on it: serialize them, e.g. on one stream.
+ * Other arguments, layouts and errors as nexus_suffix_attn.
+ */
+#define NEXUS_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+nexus_status nexus_suffix_attn_noalloc(const void *q, int32_t n_s, int32_t n_q_heads,
+                                       const nexus_kv_cache *cache, const nexus_page_table *pt,
+                                       int32_t layer, int64_t n_past, float softcap,
+                                       int32_t v_layout, float scale, void *out, void *stream);
+
+/*
  * Several suffixes over one cache in one launch (many blocks spliced into one context, each
  * re-decoding its own tail).  Sequence b has seq_len[b] queries, rows q_start[b] ..
  * q_start[b] + seq_len[b] - 1 of q and out, at positions seq_n_past[b] + i.  seq_* are HOST

@@ -503,13 +503,19 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   const bool range_major = p.n_seqs > 1;
   int64_t best_sk = kMaxSplitKeys;
   double best_cost = 1e300;
+  bool found = false;
+  const double cap = p.ws_cap == SIZE_MAX ? 1e300 : (double)p.ws_cap;
+  // workspace bytes of a sequence whose rows keep `n` partials each (none for one split)
+  auto part_bytes = [&](const AttnSeq &s, int64_t n) {
+    return n > 1 ? 4.0 * (double)n * s.len * p.n_q_heads * (p.head_dim + 2) : 0.0;
+  };
   for (int ns = 1; ns <= kMaxRanges; ++ns) {
     int64_t sk = (max_keys + ns - 1) / ns;
     sk = (sk + KT - 1) / KT * KT;
     if (sk > kMaxSplitKeys) continue;
     if (sk < kMinSplitKeysSmall && ns > 1) break;
     int64_t max_splits = 1, n_full = 0, full_len = 0, max_piece = 0, n_pieces = 0;
-    double total = 0.0, combine_bytes = 0.0;
+    double total = 0.0, combine_bytes = 0.0, ws_need = 0.0;
     for (int b = 0; b < p.n_seqs; ++b) {
       const AttnSeq &s = p.seqs[b];
       const std::vector<int64_t> &wk = tg_keys[b];
@@ -517,6 +523,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
       const int64_t skb = range_major ? sk : seq_split(keys, sk);
       const int64_t nsb = (keys + skb - 1) / skb;
       max_splits = std::max(max_splits, nsb);
+      ws_need += part_bytes(s, nsb);
       if (nsb > 1)
         combine_bytes += 8.0 * nsb * s.len * p.n_q_heads * (p.head_dim + 2) +
                          2.0 * s.len * p.n_q_heads * p.head_dim;
@@ -544,6 +551,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
       total += (seq_keys[b] + (double)pieces * kPieceOverhead) * p.n_kv_heads;
     }
     if (sk < kMinSplitKeys && ns > 1 && n_pieces > kCUs) continue;
+    if (ws_need > cap) continue;
     const double rounds_full = (double)((n_full + slots - 1) / slots);
     const double est = std::max({rounds_full * (double)(full_len + kPieceOverhead),
                                  (double)max_piece, total / (double)slots});
@@ -552,8 +560,11 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     if (cost < best_cost - 1e-9) {
       best_cost = cost;
       best_sk = sk;
+      found = true;
     }
   }
+  // under a workspace cap every plan must fit it (without one the loop always finds a plan)
+  if (!found && p.ws_cap != SIZE_MAX) return false;
   const int64_t split_keys = best_sk;
 
   // Two split classes (one suffix-like sequence): when the units of one split length leave the
@@ -568,6 +579,11 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     const int64_t slots_h = std::max<int64_t>(1, slots / p.n_kv_heads);
     const double rows_heads = (double)s.len * p.n_q_heads;
     auto split_len = [&](int64_t ns) { return seq_split(keys, (keys + ns - 1) / ns); };
+    // split count of the cut that asks for `want` splits (as the plan below makes it)
+    auto cut_count = [&](int64_t want) {
+      const int64_t kk = ((keys + want - 1) / want + KT - 1) / KT * KT;
+      return (keys + kk - 1) / kk;
+    };
     for (int64_t ns_a = 1; ns_a <= 16; ++ns_a) {
       const int64_t la = split_len(ns_a);
       if (la > kMaxSplitKeys || (la < kMinSplitKeys && ns_a > 1)) continue;
@@ -578,6 +594,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
         const int64_t ns_b = slots_h / n_b;
         const int64_t lb = split_len(ns_b);
         if (lb > kMaxSplitKeys || ns_b <= ns_a) continue;
+        if (part_bytes(s, std::max(cut_count(ns_a), cut_count(ns_b))) > cap) continue;
         const int64_t rounds_a = (n_a * ns_a + slots_h - 1) / slots_h;
         const double est = (double)rounds_a * (la + kPieceOverhead) + (double)(lb + kPieceOverhead);
         const double comb = 8.0 * rows_heads * (p.head_dim + 2) *

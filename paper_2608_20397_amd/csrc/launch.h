@@ -67,6 +67,9 @@ struct AttnLaunch {
   const AttnSeq *seqs;  // host array
   void *workspace;
   size_t workspace_bytes;
+  // Largest workspace the plan may use: the planner then only considers key splits whose
+  // partials fit (SIZE_MAX: no limit, the plan of least estimated time).
+  size_t ws_cap = SIZE_MAX;
 };
 
 // Workspace bytes an attention launch with these sequences needs.

@@ -7,6 +7,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <vector>
 
 #include "launch.h"
@@ -82,7 +83,7 @@ hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
 nexus_status prepare_attention(const void *q, int32_t n_q_heads, const nexus_kv_cache *cache,
                                const nexus_page_table *pt, int32_t layer, float softcap,
                                int32_t v_layout, float scale, void *out,
-                               const std::vector<AttnSeq> &seqs, AttnLaunch &L) {
+                               const AttnSeq *seqs, int32_t n_seqs, AttnLaunch &L) {
   nexus_status st = check_cache(cache);
   if (st) return st;
   if (!q || !out) return NEXUS_EINVAL;
@@ -101,10 +102,11 @@ nexus_status prepare_attention(const void *q, int32_t n_q_heads, const nexus_kv_
   } else if (cache->head_dim > 256) {
     return NEXUS_ESHAPE;
   }
-  if (seqs.empty() || seqs.size() > 32) return NEXUS_EINVAL;
+  if (!seqs || n_seqs < 1 || n_seqs > 32) return NEXUS_EINVAL;
   const int64_t capacity = (int64_t)pt->n_logical_pages * kPageSize;
   int64_t rows = 0;
-  for (const AttnSeq &s : seqs) {
+  for (int32_t b = 0; b < n_seqs; ++b) {
+    const AttnSeq &s = seqs[b];
     if (s.len <= 0 || s.q_start < 0) return NEXUS_EINVAL;
     if (s.n_past < 0 || s.n_past + s.len > capacity) return NEXUS_ERANGE;
     rows += s.len;
@@ -127,8 +129,8 @@ nexus_status prepare_attention(const void *q, int32_t n_q_heads, const nexus_kv_
   L.is_bf16 = bf16;
   L.scale = scale > 0.f ? scale : 1.0f / sqrtf((float)cache->head_dim);
   L.softcap = softcap;
-  L.n_seqs = (int32_t)seqs.size();
-  L.seqs = seqs.data();
+  L.n_seqs = n_seqs;
+  L.seqs = seqs;
   return NEXUS_OK;
 }
 
@@ -399,12 +401,75 @@ nexus_status nexus_suffix_attn(const void *q, int32_t n_s, int32_t n_q_heads,
                                float scale, void *out, void *workspace, size_t workspace_bytes,
                                void *stream) {
   if (n_s <= 0) return NEXUS_EINVAL;
-  std::vector<AttnSeq> seqs{AttnSeq{0, n_s, n_past}};
+  const AttnSeq seq{0, n_s, n_past};
   AttnLaunch L;
   nexus_status st = prepare_attention(q, n_q_heads, cache, pt, layer, softcap, v_layout, scale,
-                                      out, seqs, L);
+                                      out, &seq, 1, L);
   if (st) return st;
   return run_attention(L, workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+// ---- allocation-free suffix attention: the split partials live in a static device array.
+// Each GPU the library runs on holds its own copy of `scratch` (NEXUS_NOALLOC_SCRATCH_BYTES)
+// until the process ends.  In host code `scratch` names a host-side stand-in, never a device
+// address: its device address is taken once per device with hipGetSymbolAddress and kept in
+// scratch_ptr[], which is what the kernels receive.
+static __device__ __align__(256) float scratch[NEXUS_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void *scratch_ptr[kMaxDevices];   // device address of `scratch` on each device, once known
+
+// Device address of the current device's `scratch` (taken on the first call on that device,
+// with that device current).  A non-null stream must belong to the current device.
+nexus_status scratch_of_current_device(void *stream, void **ptr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return NEXUS_EHIP;
+  if (dev < 0 || dev >= kMaxDevices) return NEXUS_EINVAL;
+  if (stream) {
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice(as_stream(stream), &sdev) != hipSuccess) return NEXUS_EHIP;
+    if (sdev != dev) return NEXUS_EINVAL;
+  }
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return NEXUS_EHIP;
+    scratch_ptr[dev] = p;
+  }
+  *ptr = scratch_ptr[dev];
+  return NEXUS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+nexus_status nexus_suffix_attn_noalloc(const void *q, int32_t n_s, int32_t n_q_heads,
+                                       const nexus_kv_cache *cache, const nexus_page_table *pt,
+                                       int32_t layer, int64_t n_past, float softcap,
+                                       int32_t v_layout, float scale, void *out, void *stream) {
+  if (n_s <= 0) return NEXUS_EINVAL;
+  const AttnSeq seq{0, n_s, n_past};
+  AttnLaunch L;
+  nexus_status st = prepare_attention(q, n_q_heads, cache, pt, layer, softcap, v_layout, scale,
+                                      out, &seq, 1, L);
+  if (st) return st;
+  // the plan of least estimated time among those whose partials fit the array: the plan of
+  // nexus_suffix_attn whenever that one fits
+  L.ws_cap = NEXUS_NOALLOC_SCRATCH_BYTES;
+  const size_t need = attn_workspace_bytes(L);
+  if (need == SIZE_MAX || need > NEXUS_NOALLOC_SCRATCH_BYTES) return NEXUS_EWORKSPACE;
+  void *ws = nullptr;
+  st = scratch_of_current_device(stream, &ws);
+  if (st) return st;
+  L.workspace = ws;
+  L.workspace_bytes = NEXUS_NOALLOC_SCRATCH_BYTES;
+  return from_hip(launch_attention(L, as_stream(stream)));
 }
 
 nexus_status nexus_suffix_attn_varlen(const void *q, int32_t n_seqs, const int32_t *q_start,
@@ -418,7 +483,7 @@ nexus_status nexus_suffix_attn_varlen(const void *q, int32_t n_seqs, const int32
   for (int32_t b = 0; b < n_seqs; ++b) seqs.push_back(AttnSeq{q_start[b], seq_len[b], seq_n_past[b]});
   AttnLaunch L;
   nexus_status st = prepare_attention(q, n_q_heads, cache, pt, layer, softcap, v_layout, scale,
-                                      out, seqs, L);
+                                      out, seqs.data(), (int32_t)seqs.size(), L);
   if (st) return st;
   return run_attention(L, workspace, workspace_bytes, stream);
 }

@@ -74,6 +74,8 @@ def lib():
         "nexus_rope_append": (i32, [pC, pT, vp, vp, i32, i64, i64, vp]),
         "nexus_suffix_attn": (i32, [vp, i32, i32, pC, pT, i32, i64, f32, i32, f32, vp, vp, sz, vp]),
         "nexus_suffix_attn_workspace": (sz, [i32, i32, pC, i64]),
+        "nexus_suffix_attn_noalloc": (i32, [vp, i32, i32, pC, pT, i32, i64, f32, i32, f32, vp,
+                                            vp]),
         "nexus_suffix_attn_varlen": (i32, [vp, i32, C.POINTER(C.c_int32), C.POINTER(C.c_int32),
                                            C.POINTER(C.c_int64), i32, pC, pT, i32, f32, i32, f32,
                                            vp, vp, sz, vp]),
@@ -289,6 +291,30 @@ def suffix_attn(q: torch.Tensor, cache: PagedKVCache, layer: int, n_past: int,
                                    softcap, cache.v_layout if v_layout is None else v_layout,
                                    scale, _ptr(out), _ptr(ws), nbytes, _stream()),
            "nexus_suffix_attn")
+    return out
+
+
+def suffix_attn_noalloc(q: torch.Tensor, cache: PagedKVCache, layer: int, n_past: int,
+                        softcap: float = 0.0, v_layout: int | None = None, scale: float = 0.0,
+                        out: torch.Tensor | None = None):
+    """suffix_attn without a workspace: the split partials live in the library's static device
+    array (see nexus_suffix_attn_noalloc); with ``out`` given, nothing is allocated."""
+    n_s, hq, _ = q.shape
+    if not q.is_contiguous():
+        raise NexusError(EINVAL, "q must be contiguous")
+    if q.dtype != cache.k.dtype:
+        raise NexusError(EDTYPE, "q dtype differs from the cache")
+    if out is None:
+        out = torch.empty_like(q)
+    elif out.shape != q.shape or out.dtype != q.dtype or not out.is_contiguous():
+        raise NexusError(EINVAL, "out must be contiguous, shaped and typed like q")
+    cc, pt = cache.c(), cache.pt()
+    _on_device(("cache k", cache.k), ("q", q), ("out", out))
+    _check(lib().nexus_suffix_attn_noalloc(_ptr(q), n_s, hq, C.byref(cc), C.byref(pt), layer,
+                                           n_past, softcap,
+                                           cache.v_layout if v_layout is None else v_layout,
+                                           scale, _ptr(out), _stream()),
+           "nexus_suffix_attn_noalloc")
     return out
 
 
