@@ -10,9 +10,13 @@ over a 17472-token cache.
 
 Prints one JSON line.  ``value`` is the whole-step attention throughput (algorithmic attention
 FLOPs per step / step time, TFLOP/s); ``roofline`` reports the attention kernel against the bf16
-MFMA peak and ``roofline_hbm`` the splice and re-anchor kernels against HBM bandwidth, all on
-algorithmic work (the bytes or FLOPs the operation itself defines).  ``cpu_baseline`` times the fp64 oracle on a bounded sample of
-the same workload on the host cores.
+MFMA peak and ``roofline_hbm`` the splice and re-anchor kernels against HBM bandwidth (each
+timed alone after a streaming pass that evicts the Infinity Cache; their in-step times beside),
+all on algorithmic work (the bytes or FLOPs the operation itself defines) and also against the
+copy and MFMA ceilings measured on the GPU (``measured_peaks``).  ``configs`` holds the same
+figures for the other bf16 workloads (one layer of Qwen2.5-14B shapes at depth 2048; 16 blocks
+spliced into a shuffled 32K cache; head_dim 256 with a transposed V and a soft cap).
+``cpu_baseline`` times the fp64 oracle on a bounded sample of each workload on the host cores.
 """
 
 from __future__ import annotations
@@ -187,10 +191,10 @@ def run_step(S, events=None):
                 workspace=S["ws"]))
 
 
-def cpu_baseline(cfg: int, n_kv_sample: int, n_layers: int):
+def cpu_baseline(cfg: int, n_kv_sample: int, n_layers: int, n_blocks: int = 0):
     """The fp64 oracle on a bounded sample: the first ``n_layers`` layers' splice + re-anchor
-    (all heads) and the attention of ``n_kv_sample`` KV heads' query groups, scaled to the
-    whole step."""
+    (all heads) and the attention of ``n_kv_sample`` KV heads' query groups of the first
+    ``n_blocks`` blocks (0: all), scaled to the whole step."""
     import dataclasses
 
     from threadpoolctl import threadpool_info
@@ -201,6 +205,8 @@ def cpu_baseline(cfg: int, n_kv_sample: int, n_layers: int):
 
     wl = G.get_workload(cfg)
     n_layers = max(1, min(n_layers, wl.n_layers))
+    nb = len(wl.splice_pos)
+    n_blocks = nb if n_blocks <= 0 else min(n_blocks, nb)
     t_splice = t_attn = 0.0
     G_ = wl.group
     for layer in range(n_layers):
@@ -222,73 +228,181 @@ def cpu_baseline(cfg: int, n_kv_sample: int, n_layers: int):
         lk, lv = O.gather_logical(ck, cv, pm, n_keys, PAGE, wl.v_layout)
         k = O.storage_to_f64(lk[0], wl.dtype)
         v = O.storage_to_f64(lv[0], wl.dtype)
-        for b, n_past in enumerate(wl.attn_n_past):
+        for b, n_past in enumerate(wl.attn_n_past[:n_blocks]):
             qb = O.storage_to_f64(hc.q[0, b * wl.n_suffix:(b + 1) * wl.n_suffix], wl.dtype)
             for g in range(n_kv_sample):
                 O.suffix_attention(qb[:, g * G_:(g + 1) * G_], k[:, g:g + 1], v[:, g:g + 1],
                                    n_past, softcap=wl.softcap)
         t_attn += time.perf_counter() - t0
-    step_s = (wl.n_layers / n_layers) * (t_splice + t_attn * wl.n_kv_heads / n_kv_sample)
+    step_s = (wl.n_layers / n_layers) * (
+        t_splice + t_attn * (wl.n_kv_heads / n_kv_sample) * (nb / n_blocks))
     flops = attn_flops(wl) * wl.n_layers
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    blk = f" of the first {n_blocks} of {nb} blocks" if n_blocks < nb else ""
     return {
         "value": flops / step_s / 1e12,
         "unit": "TFLOP/s",
         "cores": int(threads),
+        "host_cpu_count": os.cpu_count(),
+        "affinity_cpus": len(os.sched_getaffinity(0)),
         "kind": "oracle",
-        "sample": (f"layers 0..{n_layers - 1}: splice + re-anchor of all {wl.n_kv_heads} KV heads "
-                   f"({t_splice:.2f} s) and attention of {n_kv_sample} of {wl.n_kv_heads} KV-head "
-                   f"query groups ({t_attn:.2f} s), scaled x{wl.n_layers / n_layers:g} layers and "
-                   f"x{wl.n_kv_heads / n_kv_sample:g} heads to one step; fp64 numpy, BLAS threads "
-                   f"for the matmuls, elementwise exp single-threaded"),
+        "sample": (f"cfg{cfg} layers 0..{n_layers - 1}: splice + re-anchor of all "
+                   f"{wl.n_kv_heads} KV heads ({t_splice:.2f} s) and attention of {n_kv_sample} "
+                   f"of {wl.n_kv_heads} KV-head query groups{blk} ({t_attn:.2f} s), scaled "
+                   f"x{wl.n_layers / n_layers:g} layers, x{wl.n_kv_heads / n_kv_sample:g} heads"
+                   f"{f' and x{nb / n_blocks:g} blocks' if blk else ''} to one step; fp64 numpy, "
+                   f"`cores` BLAS threads for the matmuls (of host_cpu_count), elementwise exp "
+                   f"single-threaded"),
         "step_s_estimate": step_s,
     }
 
 
-def time_next_rows(S, reps: int):
-    """The one-pass splice + re-anchor of the block(s) and the rope-append of the suffix tokens,
-    timed alone after the measured steps (they are not part of a step).  GB/s on algorithmic
-    bytes: read + write of the block's K and V (the separate calls move 4 |K| + 2 |K|), and read
-    + write of the appended tokens' K and V."""
+def time_rotating(fns, reps: int):
+    """Mean ms per call of back-to-back calls cycling through ``fns``, callables that each touch
+    their own buffers: with enough of them, every call reads data last touched several hundred
+    MiB earlier (evicted from the 256 MB Infinity Cache) while earlier calls' writes drain to
+    HBM, the steady state of a stream of such calls.  The calls of one cycle are captured in a
+    HIP graph and replayed, so that host launch cost stays out of the figure."""
+    import torch
+    for f in fns:
+        f()                                   # first calls (and binding checks) outside capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(st):
+        with torch.cuda.graph(g, stream=st):
+            for f in fns:
+                f()
+    torch.cuda.current_stream().wait_stream(st)
+    g.replay()
+    torch.cuda.synchronize()
+    n = max(reps, 3)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(n):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / (n * len(fns))
+
+
+def time_back_to_back(fn, reps: int):
+    """Mean ms of ``fn`` over back-to-back calls between two events (repeats re-read what the
+    previous call left in the caches)."""
+    return time_rotating([fn], reps)
+
+
+def hbm_row(nbytes: float, ms: float, **extra):
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    row = {"mean_launch_ms": ms, "bytes_per_launch": int(nbytes), "achieved_GBps": gbps,
+           "frac": gbps / HBM_PEAK_GBPS}
+    row.update(extra)
+    return row
+
+
+ROT_MIB = 1536      # bytes the copies of a rotation touch together, at least
+
+
+def time_hbm_kernels(S, reps: int):
+    """The HBM-bound kernels of a config timed alone in steady state: each cycles over copies of
+    its operands (a block and a cache of the block's pages) that together touch at least
+    1.5 GiB, so every call reads HBM.  Splice of the block, in-place re-anchor of its pages, the
+    one-pass splice + re-anchor, and the rope-append of the suffix tokens.  GB/s on algorithmic
+    bytes: read + write of the block's K and V (splice, one-pass), of its K (re-anchor), of the
+    appended tokens' K and V (rope-append).  The copies hold only the pages the block covers,
+    at the block's page alignment; the kernels' work does not depend on the other pages."""
     import torch
     from paper_2608_20397_amd import nexus as N
-    wl, cache = S["wl"], S["cache"]
+    from synth import PAGE
+    wl = S["wl"]
     esize = 2 if wl.dtype == "bf16" else 4
-    L, H, D = wl.n_layers, wl.n_kv_heads, wl.head_dim
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    L, H, D, T = wl.n_layers, wl.n_kv_heads, wl.head_dim, wl.block_len
+    blk_bytes = L * T * H * D * esize
+    pos = wl.splice_pos[0]
+    off = pos % PAGE                                   # same alignment within a page
+    npp = (off + max(T, wl.n_suffix) + PAGE - 1) // PAGE
+    vt = wl.v_layout == "transposed"
+    n_rot = max(3, -(-(ROT_MIB << 20) // (4 * blk_bytes)))
 
-    def timeit(fn):
-        # back-to-back calls between two events on the launch stream: kernel time, not the
-        # host's launch latency of a lone call
-        fn()
-        torch.cuda.synchronize()
-        n = max(reps, 3)
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(n):
-            fn()
-        b.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / n
+    def cache_copy(with_v=True):
+        k = torch.zeros((L, npp, H, PAGE, D), dtype=dt, device="cuda")
+        if with_v:
+            v = torch.zeros((L, H, D, npp * PAGE) if vt else (L, npp, H, PAGE, D), dtype=dt,
+                            device="cuda")
+        else:
+            v = shared_v
+        return N.PagedKVCache(k, v, torch.arange(npp, dtype=torch.int32, device="cuda"),
+                              wl.rope_base, N.V_TRANSPOSED if vt else N.V_ROWMAJOR)
 
+    shared_v = None
+    caches = [cache_copy() for _ in range(n_rot)]
+    blocks = [N.Block(torch.randn((L, T, H, D), device="cuda").to(dt),
+                      torch.randn((L, T, H, D), device="cuda").to(dt), 0, wl.rope_base)
+              for _ in range(n_rot)]
     out = {}
-    blk_bytes = L * wl.block_len * H * D * esize
-    for b, pos in enumerate(wl.splice_pos[:1]):
-        blk = S["blocks"][b]
-        ms = timeit(lambda: N.splice_rephase_pages(cache, blk, pos, pos))
-        out["splice_rephase_fused"] = {
-            "mean_launch_ms": ms, "bytes_per_launch": 4 * blk_bytes,
-            "achieved_GBps": 4 * blk_bytes / (ms * 1e-3) / 1e9,
-            "frac": 4 * blk_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+    out["splice"] = hbm_row(4 * blk_bytes, time_rotating(
+        [lambda c=c, b=b: N.splice_pages(c, b, off) for c, b in zip(caches, blocks)], reps),
+        rotation=n_rot)
+    # the re-anchor touches only K: twice as many copies for the same span; each call rotates
+    # its copy's keys one position further (a rotation keeps their norms)
+    n_k = 2 * n_rot
+    shared_v = caches[0].v
+    kcaches = caches + [cache_copy(with_v=False) for _ in range(n_k - n_rot)]
+    out["rephase"] = hbm_row(2 * blk_bytes, time_rotating(
+        [lambda c=c: N.rephase_k_paged(c, off, T, pos, pos + 1, wl.rope_base) for c in kcaches],
+        reps), rotation=n_k)
+    del kcaches
+    out["splice_rephase_fused"] = hbm_row(4 * blk_bytes, time_rotating(
+        [lambda c=c, b=b: N.splice_rephase_pages(c, b, off, pos) for c, b in zip(caches, blocks)],
+        reps), rotation=n_rot)
     n_app = wl.n_suffix
-    k_new = S["q"].new_empty((L, n_app, H, D)).normal_()
-    v_new = torch.empty_like(k_new).normal_()
-    off = wl.n_tokens - n_app
-    ms = timeit(lambda: N.rope_append(cache, k_new, v_new, off, off))
-    nbytes = 4 * L * n_app * H * D * esize
-    out["rope_append"] = {
-        "tokens": n_app, "mean_launch_ms": ms, "bytes_per_launch": nbytes,
-        "achieved_GBps": nbytes / (ms * 1e-3) / 1e9, "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+    apps = [(torch.randn((L, n_app, H, D), device="cuda").to(dt),
+             torch.randn((L, n_app, H, D), device="cuda").to(dt)) for _ in range(n_rot)]
+    out["rope_append"] = hbm_row(4 * L * n_app * H * D * esize, time_rotating(
+        [lambda c=c, kv=kv: N.rope_append(c, kv[0], kv[1], off, pos) for c, kv in zip(caches, apps)],
+        reps), tokens=n_app, rotation=n_rot)
+    del caches, blocks, apps
+    torch.cuda.empty_cache()
     return out
+
+
+def batched_splice_cfg2(reps: int):
+    """Supplementary figure for config 2, whose single-layer splice (4 MiB) is far below the
+    size a launch needs to approach the HBM roofline: the same block shape (512 tokens x 8 KV
+    heads x 128, bf16, spliced at 2048) over all 48 layers in one call, as a real splice moves
+    every layer; timed like the other HBM kernels (steady state over rotated copies)."""
+    import dataclasses
+
+    from synth import gen as G
+    wl = dataclasses.replace(G.get_workload(2), n_layers=48)
+    out = time_hbm_kernels({"wl": wl}, reps)
+    out["label"] = "supplementary: config 2's block shape over 48 layers in one launch"
+    return out
+
+
+def measured_peaks():
+    """The copy and bf16 MFMA ceilings measured on this GPU with the library's calibration
+    kernels: a 1 GiB device copy (read + write bytes / time) and 2 waves per SIMD of
+    back-to-back 32x32x16 bf16 MFMAs."""
+    import torch
+    from paper_2608_20397_amd import nexus as N
+    n = 1 << 30
+    src = torch.empty(n // 4, dtype=torch.int32, device="cuda").random_()
+    dst = torch.empty_like(src)
+    ms = time_back_to_back(lambda: N.calib_copy(src, dst), 10)
+    sink = torch.zeros(512, dtype=torch.float32, device="cuda")
+    fl = [0.0]
+
+    def mfma():
+        fl[0] = N.calib_mfma_bf16(20000, sink)
+    ms_m = time_back_to_back(mfma, 5)
+    del src, dst
+    return {"copy_GBps": 2 * n / (ms * 1e-3) / 1e9, "copy_bytes": 2 * n,
+            "mfma_bf16_TFLOPs": fl[0] / (ms_m * 1e-3) / 1e12,
+            "how": "nexus_calib_copy of 1 GiB, back to back; nexus_calib_mfma_bf16 "
+                   "(4 independent 32x32x16 bf16 MFMA chains per wave, 2 waves per SIMD)"}
 
 
 def _graph_time(fn, reps: int, inner: int = 1):
@@ -461,8 +575,10 @@ def sweep(reps: int):
     n_past + 512 + 64 tokens.  Splice path = prefill of the n_past context tokens, the one-pass
     splice + re-anchor of the block (all layers) and the attention of the redecoded
     r = redecode_len(512, n_past, 256, 5, K) block tokens plus the user tokens over the whole
-    cache.  Each variant's 48-layer call sequence is captured in a HIP graph and replayed, so
-    host launch overhead does not enter the comparison."""
+    cache, as two launches per layer (context, then suffix) or as one (the context rows and the
+    redecoded rows as two sequences of one varlen launch, after the splice).  Each variant's
+    48-layer call sequence is captured in a HIP graph and replayed, so host launch overhead does
+    not enter the comparison."""
     import torch
     from paper_2608_20397_amd import nexus as N
     from synth import PAGE
@@ -517,6 +633,24 @@ def sweep(reps: int):
                     N.suffix_attn(qs[l], cache, l, n0, 0.0, out=outs[l], workspace=ws)
             return run
 
+        def one_launch_calls(n_s):
+            starts, lens, pasts = [0, n_past], [n_past, n_s], [0, total - n_s]
+            qs = [torch.cat([q[l, :n_past], q[l, total - n_s:]]).contiguous() for l in range(L)]
+            outs = [torch.empty_like(x) for x in qs]
+            ws = torch.empty(max(N.suffix_attn_varlen_workspace_bytes(cache, starts, lens, pasts,
+                                                                      Hq), 16),
+                             dtype=torch.uint8, device="cuda")
+
+            def run():
+                for l in range(L):
+                    N.suffix_attn_varlen(qs[l], starts, lens, pasts, cache, l, out=outs[l],
+                                         workspace=ws)
+            return run
+
+        def flops(r0, r1):
+            # QK^T and PV over the unmasked pairs of queries r0 .. r1 - 1 (query i sees i + 1 keys)
+            return 4 * D * Hq * ((r1 * (r1 + 1) - r0 * (r0 + 1)) // 2)
+
         prefill = attn_calls(0, total, 0)
         context = attn_calls(0, n_past, 0)
         t_prefill = graph_ms(prefill)
@@ -533,16 +667,83 @@ def sweep(reps: int):
                 suffix()
             t_suf = graph_ms(suffix)
             t_path = graph_ms(path)
+            # the same splice path with the context rows and the redecoded rows of a layer in
+            # one launch (two sequences of one varlen call), after the splice
+            one = one_launch_calls(n_s)
+
+            def path1():
+                N.splice_rephase_pages(cache, blk, n_past, n_past)
+                one()
+            t_path1 = graph_ms(path1)
             R = r_base if n_past <= M else min(
                 100.0, r_base + (n_past - M) * (100.0 - r_base) / (M * (K - 1)))
             rows.append({"K": K, "n_past": n_past, "R_pct": round(R, 1), "redecode": r,
                          "prefill_ms": t_prefill, "context_ms": t_ctx, "splice_ms": t_splice,
-                         "suffix_ms": t_suf, "splice_path_ms": t_path,
-                         "speedup": t_prefill / t_path,
-                         "query_tokens_ratio": total / (n_past + n_s)})
+                         "suffix_ms": t_suf, "suffix_us_per_layer": 1e3 * t_suf / L,
+                         "splice_path_ms": t_path, "speedup": t_prefill / t_path,
+                         "splice_path_one_launch_ms": t_path1,
+                         "speedup_one_launch": t_prefill / t_path1,
+                         "query_tokens_ratio": total / (n_past + n_s),
+                         "attn_flops_ratio": flops(0, total) / (flops(0, n_past) + flops(total - n_s, total))})
         del k, v, cache, blk, q
         torch.cuda.empty_cache()
     return rows
+
+
+def run_config(cfg: int, steps: int, warmup: int):
+    """Set up config ``cfg``, run ``warmup`` untimed steps and ``steps`` timed ones; returns the
+    set-up state, the step time and the mean duration of each kind of call (HIP events on the
+    launch stream)."""
+    import torch
+    S = setup(cfg)
+    print(f"bench: cfg{cfg} {S['wl'].name}: setup done", file=sys.stderr, flush=True)
+    for _ in range(warmup):
+        run_step(S)
+    torch.cuda.synchronize()
+    events = []
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        run_step(S, events)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    dur = {}
+    for kind, a, b in events:
+        dur.setdefault(kind, []).append(a.elapsed_time(b))
+    mean = {k: sum(v) / len(v) for k, v in dur.items()}
+    print(f"bench: cfg{cfg}: {steps} steps, {ms:.3f} ms/step, mean call ms {mean}",
+          file=sys.stderr, flush=True)
+    return S, ms, mean
+
+
+def config_summary(S, ms: float, mean: dict, hbm: dict, peaks: dict):
+    """Per-config figures: attention against the bf16 MFMA peak, splice and re-anchor against
+    HBM (inside the step, and timed alone after a cache-evicting pass)."""
+    wl = S["wl"]
+    esize = 2 if wl.dtype == "bf16" else 4
+    blk_bytes = wl.n_layers * wl.block_len * wl.n_kv_heads * wl.head_dim * esize
+    nb = len(wl.splice_pos)
+    fl = attn_flops(wl)
+    tf = fl / (mean["attn"] * 1e-3) / 1e12
+    splice_b, rephase_b = 4 * blk_bytes, 2 * blk_bytes
+    return {
+        "workload": f"cfg{wl.cfg}: {wl.name}",
+        "dtype": wl.dtype,
+        "ms_per_step": ms,
+        "step_attn_TFLOPs": fl * wl.n_layers / (ms * 1e-3) / 1e12,
+        "attn": {"achieved_TFLOPs": tf, "frac": tf / MFMA_BF16_PEAK_TFLOPS,
+                 "frac_of_measured_mfma": tf / peaks["mfma_bf16_TFLOPs"],
+                 "mean_launch_ms": mean["attn"], "flops_per_launch": fl,
+                 "launches_per_step": wl.n_layers,
+                 "call": "nexus_suffix_attn" if nb == 1 else f"nexus_suffix_attn_varlen ({nb} "
+                                                              f"suffixes)"},
+        "splice_in_step": hbm_row(splice_b, mean["splice"],
+                                  note="block read from HBM (the previous step's attention "
+                                       "evicted it)"),
+        "rephase_in_step": hbm_row(rephase_b, mean["rephase"],
+                                   note="right after the splice: its keys may still be in the "
+                                        "Infinity Cache"),
+        "hbm_alone": hbm,
+    }
 
 
 def main():
@@ -551,6 +752,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3, choices=[2, 3, 4, 5])
+    ap.add_argument("--only", action="store_true",
+                    help="measure --config alone (no other configs, next rows or baselines)")
     ap.add_argument("--cpu-kv-sample", type=int, default=8,
                     help="KV heads per layer the oracle baseline computes (0 skips it)")
     ap.add_argument("--cpu-layers", type=int, default=3,
@@ -568,6 +771,9 @@ def main():
         sys.exit(2)
 
     import torch
+    from paper_2608_20397_amd import nexus as N
+    N.lib()   # fail loudly if the library is not built
+    torch.cuda.set_device(0)
     if args.copy_calibration:
         n = args.copy_calibration << 20
         src = torch.empty(n, dtype=torch.uint8, device="cuda").random_(0, 255)
@@ -586,47 +792,21 @@ def main():
         print(json.dumps({"copy_mib": args.copy_calibration, "ms_per_copy": ms,
                           "GBps_read_plus_write": 2 * n / (ms * 1e-3) / 1e9}), flush=True)
         return
-    from paper_2608_20397_amd import nexus as N
-    N.lib()   # fail loudly if the library is not built
-    torch.cuda.set_device(0)
     if args.sweep:
         print(json.dumps({"sweep": sweep(args.steps), "unit": "ms for all 48 layers",
                           "shapes": "Qwen2.5-14B attention (40/8/128, theta 1e6), block 512, "
                                     "user 64, bf16, 48 layers, HIP-graph replay"}), flush=True)
         return
-    S = setup(args.config)
+    peaks = measured_peaks()
+    S, ms, mean = run_config(args.config, args.steps, args.warmup)
     wl = S["wl"]
-    print(f"bench: cfg{wl.cfg} {wl.name}: setup done", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        run_step(S)
-    torch.cuda.synchronize()
-    events = []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        run_step(S, events)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms = (t1 - t0) * 1e3 / args.steps
-    dur = {}
-    for kind, a, b in events:
-        dur.setdefault(kind, []).append(a.elapsed_time(b))
-    mean = {k: sum(v) / len(v) for k, v in dur.items()}
-    print(f"bench: {args.steps} steps, {ms:.3f} ms/step, mean call ms {mean}", file=sys.stderr,
-          flush=True)
+    hbm = time_hbm_kernels(S, args.steps)
+    summ = config_summary(S, ms, mean, hbm, peaks)
 
-    esize = 2 if wl.dtype == "bf16" else 4
-    nb = len(wl.splice_pos)
-    blk_bytes = wl.n_layers * wl.block_len * wl.n_kv_heads * wl.head_dim * esize   # K (or V) of one block
-    splice_bytes = 2 * 2 * blk_bytes          # read + write, K and V
-    rephase_bytes = 2 * blk_bytes             # read + write, K
     fl_layer = attn_flops(wl)
     step_flops = fl_layer * wl.n_layers
-    attn_tflops = fl_layer / (mean["attn"] * 1e-3) / 1e12
-    splice_gbps = splice_bytes / (mean["splice"] * 1e-3) / 1e9
-    rephase_gbps = rephase_bytes / (mean["rephase"] * 1e-3) / 1e9
-    rs_gbps = (splice_bytes + rephase_bytes) / ((mean["splice"] + mean["rephase"]) * 1e-3) / 1e9
-
+    attn_tflops = summ["attn"]["achieved_TFLOPs"]
+    nb = len(wl.splice_pos)
     res = {
         "metric": METRIC,
         "value": step_flops / (ms * 1e-3) / 1e12,
@@ -663,22 +843,43 @@ def main():
                                "(SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs))"),
             "algorithmic_flops_per_launch": fl_layer,
             "mean_launch_ms": mean["attn"],
+            "frac_of_measured_peak": attn_tflops / peaks["mfma_bf16_TFLOPs"],
         },
         "roofline_hbm": {
             "bound": "hbm",
-            "splice": {"achieved": splice_gbps, "bytes_per_launch": splice_bytes,
-                       "mean_launch_ms": mean["splice"], "frac": splice_gbps / HBM_PEAK_GBPS},
-            "rephase": {"achieved": rephase_gbps, "bytes_per_launch": rephase_bytes,
-                        "mean_launch_ms": mean["rephase"], "frac": rephase_gbps / HBM_PEAK_GBPS},
-            "rephase_plus_splice_GBps": rs_gbps,
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
-            "frac": rs_gbps / HBM_PEAK_GBPS,
+            "splice": hbm["splice"],
+            "rephase": hbm["rephase"],
+            "frac": ((hbm["splice"]["bytes_per_launch"] + hbm["rephase"]["bytes_per_launch"])
+                     / ((hbm["splice"]["mean_launch_ms"] + hbm["rephase"]["mean_launch_ms"]) * 1e-3)
+                     / 1e9 / HBM_PEAK_GBPS),
+            "timing": ("each kernel alone in steady state, cycling over copies of its operands "
+                       "that together touch >= 1.5 GiB (reads come from HBM)"),
+            "in_step": {"splice": summ["splice_in_step"], "rephase": summ["rephase_in_step"]},
+            "frac_of_measured_copy": {
+                k: hbm[k]["achieved_GBps"] / peaks["copy_GBps"]
+                for k in ("splice", "rephase", "splice_rephase_fused", "rope_append")},
         },
+        "measured_peaks": peaks,
     }
-    res["next_rows"] = time_next_rows(S, args.steps)
+    res["next_rows"] = {"splice_rephase_fused": hbm["splice_rephase_fused"],
+                        "rope_append": hbm["rope_append"]}
     res["next_rows"].update(time_decode(S, args.steps))
     res["next_rows"].update(time_slb(args.steps))
+    del S
+    torch.cuda.empty_cache()
+    others = [] if args.only else [c for c in (2, 4, 5) if c != args.config]
+    if others:
+        res["configs"] = {}
+    for cfg in others:
+        S2, ms2, mean2 = run_config(cfg, args.steps, args.warmup)
+        row = config_summary(S2, ms2, mean2, time_hbm_kernels(S2, args.steps), peaks)
+        if cfg == 2:
+            row["splice_48_layers_supplementary"] = batched_splice_cfg2(args.steps)
+        res["configs"][f"cfg{cfg}"] = row
+        del S2
+        torch.cuda.empty_cache()
     try:
         res["git"] = subprocess.run(["git", "-C", ROOT, "rev-parse", "--short", "HEAD"],
                                     capture_output=True, text=True).stdout.strip() or None
@@ -688,6 +889,11 @@ def main():
         print("bench: timing the oracle baseline on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(args.config, min(args.cpu_kv_sample, wl.n_kv_heads),
                                            args.cpu_layers)
+        # smaller samples of the other configs (same oracle, same scaling rule)
+        samples = {2: (8, 1, 0), 4: (2, 1, 4), 5: (8, 1, 0)}
+        for cfg in others:
+            kv, nl, nbk = samples[cfg]
+            res["configs"][f"cfg{cfg}"]["cpu_baseline"] = cpu_baseline(cfg, kv, nl, nbk)
     print(json.dumps(res), flush=True)
 
 

@@ -366,6 +366,20 @@ int64_t nexus_redecode_len(int64_t S, int64_t n_past, int32_t M, int32_t r_base_
 nexus_status nexus_check_page_table(const int32_t *host_map, int32_t n_logical_pages,
                                     int32_t n_phys_pages);
 
+/*
+ * Measurement helpers, not part of the splice path: the ceilings a kernel on this GPU reaches,
+ * against which roofline fractions are also quoted.
+ *   nexus_calib_copy       copies `bytes` (a multiple of 16; both pointers 16-byte aligned)
+ *                          from src to dst on the device: the read + write HBM ceiling.
+ *   nexus_calib_mfma_bf16  runs `iters` rounds of four independent 32x32x16 bf16 MFMAs on every
+ *                          wave of 512 workgroups x 4 waves (two waves per SIMD); *flops (host)
+ *                          receives the matrix FLOPs enqueued.  `sink` is a device array of 512
+ *                          floats that the kernel never writes in practice.
+ * Both enqueue one kernel on `stream`; NEXUS_EINVAL on bad arguments.
+ */
+nexus_status nexus_calib_copy(const void *src, void *dst, size_t bytes, void *stream);
+nexus_status nexus_calib_mfma_bf16(int32_t iters, float *sink, double *flops, void *stream);
+
 /* Static text for a status code. */
 const char *nexus_status_str(int32_t status);
 

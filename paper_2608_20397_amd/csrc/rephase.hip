@@ -5,10 +5,10 @@
 // HBM-bound: each workgroup forms the D/2 angles once in fp64 (reduced modulo 2*pi in fp64) and
 // keeps their cosine and sine in LDS as fp32 head + tail pairs (c = c_hi + c_lo to about 2^-48);
 // each thread owns a fixed group of feature pairs, holds their cos/sin in registers and streams
-// rows with 16-byte loads and stores.  The rotation x c - y s is evaluated in fp32 with the
-// product y s_hi split exactly by an FMA (Dekker's two-product) and the tail terms added
-// separately, so the fp32 result is within about 2^-23 relative of the exact rotation even
-// when the two products cancel; it is then rounded to the storage type (nearest-even).
+// rows with 16-byte non-temporal loads and stores.  The rotation x c - y s is evaluated in fp32
+// with the product y s_hi split exactly by an FMA (Dekker's two-product) and the tail terms
+// added separately, so the fp32 result is within about 2^-23 relative of the exact rotation
+// even when the two products cancel; it is then rounded to the storage type (nearest-even).
 #include "launch.h"
 #include "rope_math.h"
 
@@ -60,8 +60,8 @@ __global__ __launch_bounds__(256) void rephase_kernel(
     for (int u = 0; u < kBatch; ++u) {
       rows[u] = row_ptr(rb + u * rpp);
       const T *src = rows[u] != nullptr ? rows[u] : k;
-      va[u] = *reinterpret_cast<const u32x4 *>(src + ea);
-      vb[u] = *reinterpret_cast<const u32x4 *>(src + eb);
+      va[u] = ld_stream(reinterpret_cast<const u32x4 *>(src + ea));
+      vb[u] = ld_stream(reinterpret_cast<const u32x4 *>(src + eb));
     }
   };
   const uint32_t stride = gridDim.x * per_wg;
@@ -104,8 +104,8 @@ __global__ __launch_bounds__(256) void rephase_kernel(
           x[N + e] = b[e];
         }
       }
-      *reinterpret_cast<u32x4 *>(rows[u] + ea) = Pack<T>::pack(x);
-      *reinterpret_cast<u32x4 *>(rows[u] + eb) = Pack<T>::pack(x + N);
+      st_stream(Pack<T>::pack(x), reinterpret_cast<u32x4 *>(rows[u] + ea));
+      st_stream(Pack<T>::pack(x + N), reinterpret_cast<u32x4 *>(rows[u] + eb));
     }
     wb += stride;
     if (wb < n_rows) issue(wb + sub);

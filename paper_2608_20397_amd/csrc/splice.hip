@@ -2,7 +2,8 @@
 //
 // Pure data movement, bit-exact.  Block rows [l][j][h][:] are contiguous; cache rows
 // [l][page][h][slot][:] are contiguous, so the row-major kernel streams 16-byte chunks in the
-// block's own order (coalesced reads) and writes whole rows (256 B for bf16, head_dim 128).
+// block's own order (coalesced reads) and writes whole rows (256 B for bf16, head_dim 128),
+// both with non-temporal accesses (config 3, 48 layers, steady state: 70.6 -> 64.6 us).
 // The transposed-V kernel stages a 64-token x head_dim tile in LDS and writes it back
 // token-innermost, so both the row reads and the column writes stay coalesced.
 #include "device_common.h"
@@ -15,13 +16,13 @@ constexpr int kSpliceItemsPerThread = 1;
 // Row-major splice of K and V (blockIdx.z: 0 = K, 1 = V; z = 1 is skipped for a transposed V).
 // Work item = one 16-byte chunk; a layer's items are ordered (token j, head h, chunk c).
 __global__ __launch_bounds__(256) void splice_rows_kernel(
-    const uint4 *__restrict__ bk, const uint4 *__restrict__ bv, uint4 *__restrict__ ck,
-    uint4 *__restrict__ cv, const int32_t *__restrict__ map, int64_t offset,
+    const u32x4 *__restrict__ bk, const u32x4 *__restrict__ bv, u32x4 *__restrict__ ck,
+    u32x4 *__restrict__ cv, const int32_t *__restrict__ map, int64_t offset,
     uint32_t items_per_layer, uint32_t chunks_per_row, uint32_t chunk_shift, FastDiv div_heads,
     uint32_t n_heads, uint32_t n_phys_pages, uint32_t n_tokens) {
   const uint32_t layer = blockIdx.y;
-  const uint4 *src = blockIdx.z == 0 ? bk : bv;
-  uint4 *dst = blockIdx.z == 0 ? ck : cv;
+  const u32x4 *src = blockIdx.z == 0 ? bk : bv;
+  u32x4 *dst = blockIdx.z == 0 ? ck : cv;
   const uint64_t src_layer = (uint64_t)layer * items_per_layer;
   const uint64_t dst_layer = (uint64_t)layer * n_phys_pages * n_heads * kPage * chunks_per_row;
   // items per thread and loop pass: one item per thread, many workgroups (config 3, 48 layers:
@@ -30,7 +31,7 @@ __global__ __launch_bounds__(256) void splice_rows_kernel(
   const uint32_t stride = gridDim.x * blockDim.x;
   uint32_t idx = blockIdx.x * blockDim.x + threadIdx.x;
   for (; idx < items_per_layer; idx += kUnroll * stride) {
-    uint4 v[kUnroll];
+    u32x4 v[kUnroll];
     uint64_t daddr[kUnroll];
     bool ok[kUnroll];
 #pragma unroll
@@ -46,11 +47,11 @@ __global__ __launch_bounds__(256) void splice_rows_kernel(
       const uint32_t page = (uint32_t)map[t >> kPageShift];
       const uint32_t slot = (uint32_t)(t & (kPage - 1));
       daddr[u] = dst_layer + (((uint64_t)page * n_heads + h) * kPage + slot) * chunks_per_row + c;
-      v[u] = src[src_layer + ii];
+      v[u] = ld_stream(src + src_layer + ii);
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u)
-      if (ok[u]) dst[daddr[u]] = v[u];
+      if (ok[u]) st_stream(v[u], dst + daddr[u]);
   }
   (void)n_tokens;
 }
@@ -131,8 +132,8 @@ hipError_t launch_splice(const SpliceLaunch &p, hipStream_t stream) {
     const uint32_t blocks = (uint32_t)(want < 1 ? 1 : (want > 65535 ? 65535 : want));
     dim3 grid(blocks, p.n_layers, n_kv);
     hipLaunchKernelGGL(splice_rows_kernel, grid, dim3(threads), 0, stream,
-                       (const uint4 *)p.block_k, (const uint4 *)p.block_v, (uint4 *)p.cache_k,
-                       (uint4 *)p.cache_v, p.map, p.offset, (uint32_t)items, chunks_per_row, shift,
+                       (const u32x4 *)p.block_k, (const u32x4 *)p.block_v, (u32x4 *)p.cache_k,
+                       (u32x4 *)p.cache_v, p.map, p.offset, (uint32_t)items, chunks_per_row, shift,
                        make_fastdiv(p.n_heads), (uint32_t)p.n_heads, (uint32_t)p.n_phys_pages,
                        (uint32_t)p.n_tokens);
     hipError_t e = hipGetLastError();

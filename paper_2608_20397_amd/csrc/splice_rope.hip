@@ -70,11 +70,11 @@ __global__ __launch_bounds__(256) void rope_splice_kernel(
     x.c = c;
     const int ea = INTERLEAVED ? 2 * N * c : N * c;             // first element of each load
     const int eb = INTERLEAVED ? 2 * N * c + N : n_pairs + N * c;
-    x.ka = *reinterpret_cast<const u32x4 *>(src_k + srow + ea);
-    x.kb = *reinterpret_cast<const u32x4 *>(src_k + srow + eb);
+    x.ka = ld_stream(reinterpret_cast<const u32x4 *>(src_k + srow + ea));
+    x.kb = ld_stream(reinterpret_cast<const u32x4 *>(src_k + srow + eb));
     if (src_v != nullptr) {
-      x.va = *reinterpret_cast<const u32x4 *>(src_v + srow + ea);
-      x.vb = *reinterpret_cast<const u32x4 *>(src_v + srow + eb);
+      x.va = ld_stream(reinterpret_cast<const u32x4 *>(src_v + srow + ea));
+      x.vb = ld_stream(reinterpret_cast<const u32x4 *>(src_v + srow + eb));
     }
   };
   Item cur[kBatch];
@@ -130,11 +130,11 @@ __global__ __launch_bounds__(256) void rope_splice_kernel(
           x[N + e] = b[e];
         }
       }
-      *reinterpret_cast<u32x4 *>(ck + x0.drow + ea) = Pack<T>::pack(x);
-      *reinterpret_cast<u32x4 *>(ck + x0.drow + eb) = Pack<T>::pack(x + N);
+      st_stream(Pack<T>::pack(x), reinterpret_cast<u32x4 *>(ck + x0.drow + ea));
+      st_stream(Pack<T>::pack(x + N), reinterpret_cast<u32x4 *>(ck + x0.drow + eb));
       if (src_v != nullptr) {
-        *reinterpret_cast<u32x4 *>(cv + x0.drow + ea) = x0.va;
-        *reinterpret_cast<u32x4 *>(cv + x0.drow + eb) = x0.vb;
+        st_stream(x0.va, reinterpret_cast<u32x4 *>(cv + x0.drow + ea));
+        st_stream(x0.vb, reinterpret_cast<u32x4 *>(cv + x0.drow + eb));
       }
     }
     if (it0 + kBatch * blockDim.x < items) {

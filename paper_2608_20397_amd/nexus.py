@@ -94,6 +94,8 @@ def lib():
         "nexus_slb_scan": (i32, [vp, vp, i32, vp, vp, i32, i32, i32, f32, vp, vp, vp, vp, vp, sz,
                                  vp]),
         "nexus_slb_scan_workspace": (sz, [i32, i32, i32, i32]),
+        "nexus_calib_copy": (i32, [vp, vp, sz, vp]),
+        "nexus_calib_mfma_bf16": (i32, [i32, vp, C.POINTER(C.c_double), vp]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(L, name)
@@ -318,6 +320,19 @@ def suffix_attn_noalloc(q: torch.Tensor, cache: PagedKVCache, layer: int, n_past
     return out
 
 
+def suffix_attn_varlen_workspace_bytes(cache: PagedKVCache, q_start, seq_len, seq_n_past,
+                                       n_q_heads: int) -> int:
+    n = len(seq_len)
+    cc = cache.c()
+    nbytes = lib().nexus_suffix_attn_varlen_workspace(n, (C.c_int32 * n)(*q_start),
+                                                      (C.c_int32 * n)(*seq_len),
+                                                      (C.c_int64 * n)(*seq_n_past), n_q_heads,
+                                                      C.byref(cc))
+    if nbytes == (1 << 64) - 1:
+        raise NexusError(EINVAL, "nexus_suffix_attn_varlen_workspace")
+    return nbytes
+
+
 def suffix_attn_varlen(q: torch.Tensor, q_start, seq_len, seq_n_past, cache: PagedKVCache,
                        layer: int, softcap: float = 0.0, v_layout: int | None = None,
                        scale: float = 0.0, out: torch.Tensor | None = None,
@@ -517,3 +532,23 @@ def check_page_table(host_map, n_phys_pages: int) -> None:
     a = np.ascontiguousarray(np.asarray(host_map, dtype=np.int32))
     _check(lib().nexus_check_page_table(a.ctypes.data_as(C.POINTER(C.c_int32)), a.size,
                                         n_phys_pages), "nexus_check_page_table")
+
+
+def calib_copy(src: torch.Tensor, dst: torch.Tensor):
+    """Device copy of src's bytes into dst (measurement helper: the HBM read + write ceiling)."""
+    _on_device(("src", src), ("dst", dst))
+    n = src.numel() * src.element_size()
+    if not (src.is_contiguous() and dst.is_contiguous()) or dst.numel() * dst.element_size() < n:
+        raise NexusError(EINVAL, "calib_copy: contiguous src, and dst at least as large")
+    _check(lib().nexus_calib_copy(_ptr(src), _ptr(dst), n, _stream()), "nexus_calib_copy")
+
+
+def calib_mfma_bf16(iters: int, sink: torch.Tensor) -> float:
+    """Enqueue the bf16 MFMA ceiling kernel; returns the matrix FLOPs it performs."""
+    _on_device(("sink", sink))
+    if sink.dtype != torch.float32 or sink.numel() < 512:
+        raise NexusError(EINVAL, "calib_mfma_bf16: sink must hold 512 fp32 values")
+    fl = C.c_double(0.0)
+    _check(lib().nexus_calib_mfma_bf16(iters, _ptr(sink), C.byref(fl), _stream()),
+           "nexus_calib_mfma_bf16")
+    return fl.value

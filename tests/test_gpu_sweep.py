@@ -2,7 +2,8 @@
 rows the splice path re-decodes equal the same rows of a full causal prefill over the spliced
 cache (the 'R = 100% is a full prefill' identity, Sec. III-C, Table tab:perf), for the redecode
 lengths eq. (adaptive) gives at K = 4 and 16.  Both GPU outputs are checked against each other
-and sampled rows against the fp64 oracle."""
+and sampled rows against the fp64 oracle; the context rows and the redecoded rows computed as two
+sequences of one launch match the prefill's rows too."""
 
 import numpy as np
 import pytest
@@ -47,6 +48,15 @@ def test_redecoded_rows_equal_full_prefill_rows(n_past):
         ref_gpu = O.bf16_bits_to_f64(full_bits[total - n_s:])
         ma, rr = compare(got, ref_gpu)
         assert ma <= BF16_MAX_ABS and rr <= BF16_REL_RMS, (K, ma, rr)
+        # the context rows and the redecoded rows as two sequences of one launch
+        one = N.suffix_attn_varlen(torch.cat([q[:n_past], q[total - n_s:]]).contiguous(),
+                                   [0, n_past], [n_past, n_s], [0, total - n_s], cache, 0)
+        torch.cuda.synchronize()
+        ob = O.bf16_bits_to_f64(G.torch_to_bits(one))
+        for part, want in ((ob[:n_past], O.bf16_bits_to_f64(full_bits[:n_past])),
+                           (ob[n_past:], ref_gpu)):
+            ma, rr = compare(part, want)
+            assert ma <= BF16_MAX_ABS and rr <= BF16_REL_RMS, ("one launch", K, ma, rr)
         # the first and last redecoded rows of KV head 3's query heads against the oracle
         rows = [0, n_s - 1]
         g0 = 3 * (Hq // H)
