@@ -445,7 +445,8 @@ struct KernelShape {
 };
 
 KernelShape kernel_shape(const AttnLaunch &p) {
-  if (p.head_dim == 128 && !p.v_transposed) return {kQB, 64, 2};
+  if (p.head_dim == 128 && !p.v_transposed) return {kQB, 64, 2};   // LDS-DMA kernel
+  if (p.head_dim == 256 && p.v_transposed) return {kQB, 32, 2};    // LDS-DMA kernel
   return {kQB, key_tile_for(p.head_dim), p.head_dim >= 256 ? 1 : 2};
 }
 
@@ -712,6 +713,8 @@ void dispatch_main(const AttnArgs &args, const AttnPlan &plan, int n_kv, bool vt
 hipError_t launch_attention_f32(const AttnLaunch &p, hipStream_t stream);
 hipError_t launch_attn_d128_dma(const AttnArgs &args, const AttnPlan &plan, int n_kv, bool cap,
                                 hipStream_t stream);
+hipError_t launch_attn_d256_vt(const AttnArgs &args, const AttnPlan &plan, int n_kv, bool cap,
+                               hipStream_t stream);
 
 size_t attn_workspace_bytes(const AttnLaunch &p) {
   if (!p.is_bf16) return 0;
@@ -741,6 +744,7 @@ hipError_t launch_attention(const AttnLaunch &p, hipStream_t stream) {
   args.scale_log2 = p.scale * log2e;
   args.cap_in = p.softcap > 0.f ? p.scale / p.softcap : 0.f;
   args.cap_out = p.softcap * log2e;
+  args.cap_k = p.softcap > 0.f ? 2.0f * p.scale * log2e / p.softcap : 0.f;
   const bool cap = p.softcap > 0.f;
   switch (p.head_dim) {
     case 64: dispatch_main<64, 64>(args, plan, p.n_kv_heads, p.v_transposed, cap, stream); break;
@@ -752,7 +756,14 @@ hipError_t launch_attention(const AttnLaunch &p, hipStream_t stream) {
         dispatch_main<128, 64>(args, plan, p.n_kv_heads, p.v_transposed, cap, stream);
       }
       break;
-    case 256: dispatch_main<256, 32>(args, plan, p.n_kv_heads, p.v_transposed, cap, stream); break;
+    case 256:
+      if (p.v_transposed) {
+        const hipError_t e = launch_attn_d256_vt(args, plan, p.n_kv_heads, cap, stream);
+        if (e != hipSuccess) return e;
+      } else {
+        dispatch_main<256, 32>(args, plan, p.n_kv_heads, p.v_transposed, cap, stream);
+      }
+      break;
     default: return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();

@@ -138,12 +138,20 @@ struct AttnArgs {
   float scale_log2;     // scale * log2(e)
   float cap_in;         // scale / softcap
   float cap_out;        // softcap * log2(e)
+  float cap_k;          // 2 * scale * log2(e) / softcap
 };
 
 __device__ __forceinline__ float tanh_fast(float x) {
   // tanh x = 1 - 2 / (e^{2x} + 1); exp2 overflow to +inf gives 1, underflow to 0 gives -1.
   const float e = fast_exp2(x * 2.8853900817779268f);  // 2 / ln 2
   return 1.0f - 2.0f * __builtin_amdgcn_rcpf(e + 1.0f);
+}
+
+// The soft cap through r = 1 / (2^(s cap_k) + 1): tanh(s scale / cap) = 1 - 2 r, so the capped
+// score in log2 units is cap_out (1 - 2 r), decreasing in r (2^.. overflowing to +inf gives
+// r = 0, the cap itself; underflowing to 0 gives r = 1).
+__device__ __forceinline__ float cap_r(float s, float cap_k) {
+  return __builtin_amdgcn_rcpf(fast_exp2(s * cap_k) + 1.0f);
 }
 
 // key index within a 16-key group -> its position in the V^T tile (swap bits 2 and 3)

@@ -358,6 +358,7 @@ size_t nexus_suffix_attn_workspace(int32_t n_s, int32_t n_q_heads, const nexus_k
   L.n_kv_heads = cache->n_kv_heads;
   L.n_q_heads = n_q_heads;
   L.head_dim = cache->head_dim;
+  L.v_transposed = cache->v_layout == NEXUS_V_TRANSPOSED;   // the kernel (and plan) depend on it
   L.is_bf16 = cache->dtype == NEXUS_BF16;
   L.n_seqs = 1;
   L.seqs = seqs.data();
@@ -379,6 +380,7 @@ size_t nexus_suffix_attn_varlen_workspace(int32_t n_seqs, const int32_t *q_start
   L.n_kv_heads = cache->n_kv_heads;
   L.n_q_heads = n_q_heads;
   L.head_dim = cache->head_dim;
+  L.v_transposed = cache->v_layout == NEXUS_V_TRANSPOSED;
   L.is_bf16 = cache->dtype == NEXUS_BF16;
   L.n_seqs = n_seqs;
   L.seqs = seqs.data();

@@ -127,6 +127,19 @@ EDGE = {
                                             n_suffix=90),
     "fp32 transposed V G=2": dict(base_cfg=1, n_ctx=500, block_len=64, n_user=10, n_suffix=40,
                                   n_q_heads=4, n_kv_heads=2, v_layout="transposed", softcap=3.0),
+    # head_dim 256 with a transposed V (the LDS-DMA kernel): tails that end inside a page, over
+    # the NaN sentinel of unwritten slots, and the plan's extremes
+    "D256 transposed: single query": dict(base_cfg=5, n_ctx=300, block_len=40, n_user=0,
+                                          n_suffix=1),
+    "D256 transposed: no past": dict(base_cfg=5, n_ctx=0, block_len=50, n_user=0, n_suffix=50),
+    "D256 transposed: ragged, no cap": dict(base_cfg=5, n_ctx=1001, block_len=77, n_user=3,
+                                            n_suffix=61, softcap=0.0),
+    "D256 transposed: many splits": dict(base_cfg=5, n_ctx=20000, block_len=16, n_user=1,
+                                         n_suffix=9),
+    "D256 transposed: G=1": dict(base_cfg=5, n_ctx=2000, block_len=100, n_user=0, n_suffix=100,
+                                 n_q_heads=8),
+    "D256 transposed: G=5, shuffled": dict(base_cfg=5, n_ctx=3000, block_len=333, n_user=7,
+                                           n_suffix=200, n_q_heads=40, shuffled_pages=True),
 }
 
 

@@ -4,7 +4,7 @@ nexus_suffix_attn (caller workspace), through the C ABI.
 Calls in a row on one GPU share the array: a long suffix whose workspace plan does not fit the
 array (Qwen2.5-14B shapes, 1088 queries at depth 16384: a capped plan, so within the bf16
 attention tolerance of the workspace call), then a shorter one whose plan fits (192 queries at
-2432: bit-identical), then head_dim 256 with a transposed V and a soft cap (512 queries at 8704:
+2432: bit-identical), then head_dim 256 with a transposed V and a soft cap (256 queries at 1792:
 bit-identical), and a suffix no plan fits into the array (refused, nothing written).
 """
 
@@ -69,11 +69,11 @@ def test_noalloc_matches_workspace_call_twice_then_smaller():
 
 
 def test_noalloc_head_dim_256_transposed_softcap_is_bit_identical():
-    cache, q = _case(72, 16, 8, 256, 8704, 512, v_layout=N.V_TRANSPOSED, k_std=3.0, base=1e4)
-    assert 0 < N.suffix_attn_workspace_bytes(cache, 512, 16, 8704) <= 64 << 20
-    ref = N.suffix_attn(q, cache, 0, 8704, softcap=50.0)
+    cache, q = _case(72, 16, 8, 256, 1792, 256, v_layout=N.V_TRANSPOSED, k_std=3.0, base=1e4)
+    assert 0 < N.suffix_attn_workspace_bytes(cache, 256, 16, 1792) <= 64 << 20
+    ref = N.suffix_attn(q, cache, 0, 1792, softcap=50.0)
     got = torch.full_like(q, float("nan"))
-    N.suffix_attn_noalloc(q, cache, 0, 8704, softcap=50.0, out=got)
+    N.suffix_attn_noalloc(q, cache, 0, 1792, softcap=50.0, out=got)
     torch.cuda.synchronize()
     assert torch.equal(got.view(torch.int16), ref.view(torch.int16))
 
