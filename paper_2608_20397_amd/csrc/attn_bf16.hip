@@ -382,7 +382,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a, con
   const SeqPlan sp = plan.seq[b];
   const int row = rowg - sp.row_begin;
   // the split count of this row's task group (task order: query block major, head minor)
-  const int n_splits = group_splits(sp, ((row / kQB) * a.group + head % a.group) / kWaves);
+  const int n_splits = group_splits(sp, ((row / plan.qpw) * a.group + head % a.group) / plan.waves);
   if (n_splits == 1) return;
   const int64_t pstep = (int64_t)sp.len * a.n_q_heads;         // partial rows per split
   const int64_t prow0 = (int64_t)row * a.n_q_heads + head;
@@ -438,16 +438,19 @@ namespace {
 
 int key_tile_for(int head_dim) { return head_dim >= 256 ? 32 : 64; }
 
-// Geometry of the kernel that serves a launch: queries per wave task, key tile, and how many
-// of its workgroups are resident per CU.
+// Geometry of the kernel that serves a launch: queries per wave task, key tile, how many of its
+// workgroups are resident per CU, wave tasks per workgroup, and the plan's time per key of one
+// workgroup (us, measured).
 struct KernelShape {
-  int qpw, key_tile, wgs_per_cu;
+  int qpw, key_tile, wgs_per_cu, waves;
+  double us_per_key;
 };
 
 KernelShape kernel_shape(const AttnLaunch &p) {
-  if (p.head_dim == 128 && !p.v_transposed) return {kQB, 64, 2};   // LDS-DMA kernel
-  if (p.head_dim == 256 && p.v_transposed) return {kQB, 32, 2};    // LDS-DMA kernel
-  return {kQB, key_tile_for(p.head_dim), p.head_dim >= 256 ? 1 : 2};
+  if (p.head_dim == 128 && !p.v_transposed) return {kQB, 64, 2, kWaves, 0.03};   // LDS DMA
+  if (p.head_dim == 256 && p.v_transposed) return {kQB, 32, 2, kWaves, 0.06};   // LDS DMA
+  return {kQB, key_tile_for(p.head_dim), p.head_dim >= 256 ? 1 : 2, kWaves,
+          0.03 * p.head_dim / 128.0};
 }
 
 constexpr int kCUs = 256;
@@ -457,8 +460,8 @@ constexpr int kCUs = 256;
 // The split length is chosen to minimise an estimate of the launch time: the critical path over
 // the resident workgroup slots (the longest piece of work, the total work spread over the slots,
 // and the rounds that the near-full-length pieces need: uniform suffix shapes are decided by the
-// the latter, causal prefills by the former two) at about 0.03 us per key per workgroup for
-// head_dim 128 (measured), plus, when keys are split, the combine: writing and reading the fp32
+// the latter, causal prefills by the former two) at the kernel's measured time per key of one
+// workgroup (KernelShape), plus, when keys are split, the combine: writing and reading the fp32
 // partials at about 4 TB/s and one more launch.  A piece's work is its keys plus a fixed 128 for
 // its prologue and epilogue.
 bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
@@ -474,6 +477,8 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   constexpr int64_t kMinSplitKeys = 512, kMinSplitKeysSmall = 256;
   plan = AttnPlan{};
   plan.n_seqs = p.n_seqs;
+  plan.qpw = ks.qpw;
+  plan.waves = ks.waves;
   int64_t max_keys = 0;
   for (int b = 0; b < p.n_seqs; ++b)
     max_keys = std::max<int64_t>(max_keys, p.seqs[b].n_past + p.seqs[b].len);
@@ -491,10 +496,10 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   for (int b = 0; b < p.n_seqs; ++b) {
     const AttnSeq &s = p.seqs[b];
     const int n_tasks = n_tasks_of(s);
-    const int n_tg = (n_tasks + kWaves - 1) / kWaves;
+    const int n_tg = (n_tasks + ks.waves - 1) / ks.waves;
     tg_keys[b].resize(n_tg);
     for (int tg = 0; tg < n_tg; ++tg) {
-      const int last_task = std::min(tg * kWaves + kWaves - 1, n_tasks - 1);
+      const int last_task = std::min(tg * ks.waves + ks.waves - 1, n_tasks - 1);
       tg_keys[b][tg] = s.n_past + std::min((last_task / G + 1) * ks.qpw, s.len);
       seq_keys[b] += (double)tg_keys[b][tg];
     }
@@ -556,8 +561,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     const double rounds_full = (double)((n_full + slots - 1) / slots);
     const double est = std::max({rounds_full * (double)(full_len + kPieceOverhead),
                                  (double)max_piece, total / (double)slots});
-    const double cost = est * 0.03 * p.head_dim / 128.0 +
-                        (max_splits > 1 ? combine_bytes / 4.0e6 + 8.0 : 0.0);
+    const double cost = est * ks.us_per_key + (max_splits > 1 ? combine_bytes / 4.0e6 + 8.0 : 0.0);
     if (cost < best_cost - 1e-9) {
       best_cost = cost;
       best_sk = sk;
@@ -601,7 +605,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
         const double comb = 8.0 * rows_heads * (p.head_dim + 2) *
                                 (double)(n_a * ns_a + n_b * ns_b) / (double)n_tg +
                             2.0 * rows_heads * p.head_dim;
-        const double cost = est * 0.03 * p.head_dim / 128.0 + comb / 4.0e6 + 8.0;
+        const double cost = est * ks.us_per_key + comb / 4.0e6 + 8.0;
         if (cost < best_cost - 1e-9) {
           best_cost = cost;
           two_n_a = n_a;
@@ -623,7 +627,8 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     sp.row_begin = rows;
     sp.first_unit = unit;
     sp.n_tasks = G * ((s.len + ks.qpw - 1) / ks.qpw);
-    const int n_tg = (sp.n_tasks + kWaves - 1) / kWaves;
+    const int n_tg = (sp.n_tasks + ks.waves - 1) / ks.waves;
+    sp.n_tg = n_tg;
     const int64_t keys = s.n_past + s.len;
     int64_t ns = (keys + split_keys - 1) / split_keys;
     if (ns < 1) ns = 1;
@@ -675,7 +680,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     plan.tg_prefix[0] = 0;
     for (int i = 0; i < p.n_seqs; ++i) {
       const SeqPlan &sp = plan.seq[plan.order[i]];
-      plan.tg_prefix[i + 1] = plan.tg_prefix[i] + (sp.n_tasks + kWaves - 1) / kWaves;
+      plan.tg_prefix[i + 1] = plan.tg_prefix[i] + sp.n_tg;
     }
     plan.n_ranges = plan.seq[plan.order[0]].n_splits;
     if (plan.n_ranges > kMaxRanges) return false;

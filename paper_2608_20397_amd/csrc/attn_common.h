@@ -6,8 +6,8 @@
 namespace nexus {
 
 constexpr int kMaxSeqs = 32;
-constexpr int kWaves = 4;
-constexpr int kQB = 32;   // queries per wave task
+constexpr int kWaves = 4;   // wave tasks per workgroup of the 32-query kernels
+constexpr int kQB = 32;     // queries per wave task of the 32-query kernels
 constexpr int kMaxSplitKeys = 32768;   // keys one workgroup covers at most (LDS page table)
 
 struct SeqPlan {
@@ -16,7 +16,8 @@ struct SeqPlan {
   int64_t n_past;      // position of the first query
   int32_t row_begin;   // prefix sum of len over sequences (combine indexing)
   int32_t first_unit;  // first (task group, split) unit of this sequence
-  int32_t n_tasks;     // group * ceil(len / 32)
+  int32_t n_tasks;     // group * ceil(len / queries per task)
+  int32_t n_tg;        // task groups: ceil(n_tasks / tasks per workgroup)
   int32_t n_splits;
   int32_t split_keys;  // keys per split, a multiple of the key tile
   int32_t longest_first;  // dispatch task groups last-first (causal prefill: n_past < len)
@@ -55,15 +56,13 @@ __device__ __forceinline__ UnitWork unit_work(const SeqPlan &sp, int u) {
   }
   // prefill-like sequences take their task groups in reverse: later queries see more keys, so
   // the longest workgroups are dispatched first and the launch does not end on them
-  const int n_tg = (sp.n_tasks + kWaves - 1) / kWaves;
-  w.tgrp = sp.longest_first ? n_tg - 1 - di : di;
+  w.tgrp = sp.longest_first ? sp.n_tg - 1 - di : di;
   w.k_begin = w.split * w.split_keys;
   return w;
 }
 // Split count of task group `tgrp`.
 __device__ __forceinline__ int group_splits(const SeqPlan &sp, int tgrp) {
-  const int n_tg = (sp.n_tasks + kWaves - 1) / kWaves;
-  const int di = sp.longest_first ? n_tg - 1 - tgrp : tgrp;
+  const int di = sp.longest_first ? sp.n_tg - 1 - tgrp : tgrp;
   return di < sp.n_tg_a ? sp.n_splits : sp.n_splits_b;
 }
 
@@ -77,6 +76,8 @@ constexpr int kMaxRanges = 64;
 struct AttnPlan {
   SeqPlan seq[kMaxSeqs];
   int32_t n_seqs;
+  int32_t qpw;                                // queries per wave task
+  int32_t waves;                              // wave tasks per workgroup
   int32_t units_per_head;
   int32_t total_rows;
   int32_t any_split;
@@ -117,9 +118,8 @@ __device__ __forceinline__ UnitLoc locate_unit(const AttnPlan &plan, int unit) {
   }
   const int b = plan.order[i0];
   const int di = local - plan.tg_prefix[i0];
-  const int n_tg = (plan.seq[b].n_tasks + kWaves - 1) / kWaves;
   loc.seq = b;
-  loc.w.tgrp = plan.seq[b].longest_first ? n_tg - 1 - di : di;
+  loc.w.tgrp = plan.seq[b].longest_first ? plan.seq[b].n_tg - 1 - di : di;
   loc.w.split = lo;
   loc.w.split_keys = plan.seq[b].split_keys;
   loc.w.n_splits = plan.seq[b].n_splits;
