@@ -36,12 +36,20 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 HBM_PEAK_GBPS = 8000.0           # MI355X HBM3E
 METRIC = "suffix-redecode attn TFLOP/s + re-phase/splice GB/s, % of MI355X roofline"
 
-# Measured HBM traffic of one attention call (rocprofv3 FETCH_SIZE / WRITE_SIZE, scaled by a
-# plain copy), valid only for the kernel sources it was taken on.
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_attn_cfg3_qwen14b.txt")
-MFMA_FILE = os.path.join(ROOT, "profiles", "mfma_util_attn_cfg3_qwen14b.txt")
-ATTN_SOURCES = ["attn_bf16_dma.hip", "attn_bf16.hip", "attn_common.h", "device_common.h",
-                "launch.h"]
+# Committed counter summaries of one attention call per config (rocprofv3 FETCH_SIZE /
+# WRITE_SIZE scaled by reference kernels of known bytes, and the MFMA / VALU / LDS counters),
+# valid only for the kernel sources they were taken on.
+PROFILE_TAG = {3: "qwen14b", 4: "qwen14b_16blocks", 5: "softcap_d256"}
+ATTN_SOURCES = ["attn_bf16_dma.hip", "attn_bf16_d256.hip", "attn_bf16.hip", "attn_common.h",
+                "attn_dma.h", "device_common.h", "launch.h"]
+
+
+def traffic_file(cfg: int) -> str:
+    return os.path.join(ROOT, "profiles", f"hbm_traffic_attn_cfg{cfg}_{PROFILE_TAG.get(cfg, '')}.txt")
+
+
+def mfma_file(cfg: int) -> str:
+    return os.path.join(ROOT, "profiles", f"mfma_util_attn_cfg{cfg}_{PROFILE_TAG.get(cfg, '')}.txt")
 
 
 def attn_sources_sha() -> str:
@@ -73,7 +81,7 @@ def counter_summary(path: str, cfg: int):
 def measured_traffic(cfg: int):
     """Bytes per attention call (FETCH_SIZE + WRITE_SIZE, copy-scaled) from the committed
     counter summary, or None."""
-    kv = counter_summary(TRAFFIC_FILE, cfg)
+    kv = counter_summary(traffic_file(cfg), cfg)
     try:
         return int(kv["traffic_bytes_per_launch"]) if kv else None
     except (KeyError, ValueError):
@@ -84,7 +92,7 @@ def measured_mfma_busy(cfg: int):
     """Fraction of SIMD cycles with the MFMA pipe busy in the attention kernel
     (SQ_VALU_MFMA_BUSY_CYCLES over GRBM_GUI_ACTIVE x SIMDs) from the committed counter
     summary, or None."""
-    kv = counter_summary(MFMA_FILE, cfg)
+    kv = counter_summary(mfma_file(cfg), cfg)
     try:
         return float(kv["mfma_busy_frac"]) if kv else None
     except (KeyError, ValueError):
@@ -733,6 +741,8 @@ def config_summary(S, ms: float, mean: dict, hbm: dict, peaks: dict):
         "attn": {"achieved_TFLOPs": tf, "frac": tf / MFMA_BF16_PEAK_TFLOPS,
                  "frac_of_measured_mfma": tf / peaks["mfma_bf16_TFLOPs"],
                  "mean_launch_ms": mean["attn"], "flops_per_launch": fl,
+                 "traffic": measured_traffic(wl.cfg),
+                 "mfma_busy": measured_mfma_busy(wl.cfg),
                  "launches_per_step": wl.n_layers,
                  "call": "nexus_suffix_attn" if nb == 1 else f"nexus_suffix_attn_varlen ({nb} "
                                                               f"suffixes)"},
@@ -754,6 +764,14 @@ def main():
     ap.add_argument("--config", type=int, default=3, choices=[2, 3, 4, 5])
     ap.add_argument("--only", action="store_true",
                     help="measure --config alone (no other configs, next rows or baselines)")
+    ap.add_argument("--step-only", action="store_true",
+                    help="run the steps of --config and print their times only (no peaks, "
+                         "kernels timed alone, next rows or baselines): the command the counter "
+                         "passes profile")
+    ap.add_argument("--hbm-only", action="store_true",
+                    help="time only the HBM-bound kernels of --config (splice, re-anchor, "
+                         "one-pass splice + re-anchor, rope-append) in steady state and print "
+                         "them: the command their counter passes profile")
     ap.add_argument("--cpu-kv-sample", type=int, default=8,
                     help="KV heads per layer the oracle baseline computes (0 skips it)")
     ap.add_argument("--cpu-layers", type=int, default=3,
@@ -762,8 +780,9 @@ def main():
                     help="only run the depth-adaptive sweep (attention-only prefill vs splice "
                          "path over context depths, K = 4 and 16), print it as JSON, then exit")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
-                    help="only time a plain device copy of MIB MiB (HBM reference and the "
-                         "scale of the FETCH_SIZE / WRITE_SIZE counters), then exit")
+                    help="only time a plain device copy of MIB MiB and a stream of the same "
+                         "bytes into LDS through LDS DMA loads (HBM references and the scales "
+                         "of the FETCH_SIZE / WRITE_SIZE counters), then exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: runs on one GPU only (the library has no multi-GPU path); use --gpus 1",
@@ -789,13 +808,36 @@ def main():
         b.record()
         torch.cuda.synchronize()
         ms = a.elapsed_time(b) / reps
+        # the same bytes streamed into LDS with the attention kernels' DMA loads
+        for _ in range(3):
+            N.calib_lds_dma(src)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(reps):
+            N.calib_lds_dma(src)
+        b.record()
+        torch.cuda.synchronize()
+        ms_dma = a.elapsed_time(b) / reps
         print(json.dumps({"copy_mib": args.copy_calibration, "ms_per_copy": ms,
-                          "GBps_read_plus_write": 2 * n / (ms * 1e-3) / 1e9}), flush=True)
+                          "GBps_read_plus_write": 2 * n / (ms * 1e-3) / 1e9,
+                          "ms_per_lds_dma_read": ms_dma,
+                          "GBps_lds_dma_read": n / (ms_dma * 1e-3) / 1e9}), flush=True)
         return
     if args.sweep:
         print(json.dumps({"sweep": sweep(args.steps), "unit": "ms for all 48 layers",
                           "shapes": "Qwen2.5-14B attention (40/8/128, theta 1e6), block 512, "
                                     "user 64, bf16, 48 layers, HIP-graph replay"}), flush=True)
+        return
+    if args.hbm_only:
+        from synth import gen as G
+        print(json.dumps({"config": args.config,
+                          "hbm": time_hbm_kernels({"wl": G.get_workload(args.config)},
+                                                  args.steps)}), flush=True)
+        return
+    if args.step_only:
+        _, ms, mean = run_config(args.config, args.steps, args.warmup)
+        print(json.dumps({"config": args.config, "ms_per_step": ms, "mean_call_ms": mean}),
+              flush=True)
         return
     peaks = measured_peaks()
     S, ms, mean = run_config(args.config, args.steps, args.warmup)

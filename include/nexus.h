@@ -375,10 +375,15 @@ nexus_status nexus_check_page_table(const int32_t *host_map, int32_t n_logical_p
  *                          wave of 512 workgroups x 4 waves (two waves per SIMD); *flops (host)
  *                          receives the matrix FLOPs enqueued.  `sink` is a device array of 512
  *                          floats that the kernel never writes in practice.
- * Both enqueue one kernel on `stream`; NEXUS_EINVAL on bad arguments.
+ *   nexus_calib_lds_dma    reads `bytes` (a multiple of 16384; src 16-byte aligned) from src
+ *                          into LDS with the LDS DMA loads the attention kernels use and writes
+ *                          nothing: the reference against which the memory counters' reading of
+ *                          those loads is scaled.
+ * Each enqueues one kernel on `stream`; NEXUS_EINVAL on bad arguments.
  */
 nexus_status nexus_calib_copy(const void *src, void *dst, size_t bytes, void *stream);
 nexus_status nexus_calib_mfma_bf16(int32_t iters, float *sink, double *flops, void *stream);
+nexus_status nexus_calib_lds_dma(const void *src, size_t bytes, void *stream);
 
 /* Static text for a status code. */
 const char *nexus_status_str(int32_t status);

@@ -6,8 +6,11 @@
 //     stream);
 //   * calib_mfma_kernel: v_mfma_f32_32x32x16_bf16 back to back on four independent accumulators
 //     per wave, two waves per SIMD (the dense bf16 matrix ceiling at the clock the chip holds
-//     under that load).
-#include "device_common.h"
+//     under that load);
+//   * calib_lds_dma_kernel: streams a buffer into LDS with global_load_lds_dwordx4, the load of
+//     the attention kernels' K/V tiles, 16 KiB per workgroup and round: the bytes it reads are
+//     known, so the memory counters' reading of such loads can be scaled against it.
+#include "attn_dma.h"
 #include "nexus.h"
 
 namespace nexus {
@@ -56,6 +59,26 @@ __global__ __launch_bounds__(256) void calib_mfma_kernel(int iters, float *sink)
   if (s == -1.0e30f) sink[blockIdx.x] = s;
 }
 
+constexpr uint32_t kDmaChunk = 16384;   // bytes per workgroup and round
+
+__global__ __launch_bounds__(256) void calib_lds_dma_kernel(const char *__restrict__ src,
+                                                            uint64_t n_chunks) {
+  __shared__ __align__(1024) char buf[kDmaChunk];
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const uint32_t dst = (uint32_t)(uintptr_t)buf + wave * 4096;
+  const uint32_t voff = (uint32_t)lane * 16;
+  for (uint64_t c = blockIdx.x; c < n_chunks; c += gridDim.x) {
+    const char *p = src + c * kDmaChunk + wave * 4096;
+    dma_s<0>(dst, p, voff);
+    dma_s<1024>(dst, p, voff);
+    dma_s<2048>(dst, p, voff);
+    dma_s<3072>(dst, p, voff);
+    wait_vm<0>();
+    tile_barrier();   // the buffer is refilled next round
+  }
+}
+
 }  // namespace nexus
 
 using namespace nexus;
@@ -79,6 +102,15 @@ nexus_status nexus_calib_mfma_bf16(int32_t iters, float *sink, double *flops, vo
   hipLaunchKernelGGL(calib_mfma_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream, iters,
                      sink);
   *flops = (double)blocks * 4 /* waves */ * iters * kCalibChains * (2.0 * 32 * 32 * 16);
+  return hipGetLastError() == hipSuccess ? NEXUS_OK : NEXUS_EHIP;
+}
+
+nexus_status nexus_calib_lds_dma(const void *src, size_t bytes, void *stream) {
+  if (!src || bytes == 0 || bytes % kDmaChunk || ((uintptr_t)src & 15)) return NEXUS_EINVAL;
+  const uint64_t chunks = bytes / kDmaChunk;
+  const uint32_t blocks = (uint32_t)(chunks < 2048 ? chunks : 2048);
+  hipLaunchKernelGGL(calib_lds_dma_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream,
+                     (const char *)src, chunks);
   return hipGetLastError() == hipSuccess ? NEXUS_OK : NEXUS_EHIP;
 }
 

@@ -96,6 +96,7 @@ def lib():
         "nexus_slb_scan_workspace": (sz, [i32, i32, i32, i32]),
         "nexus_calib_copy": (i32, [vp, vp, sz, vp]),
         "nexus_calib_mfma_bf16": (i32, [i32, vp, C.POINTER(C.c_double), vp]),
+        "nexus_calib_lds_dma": (i32, [vp, sz, vp]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(L, name)
@@ -541,6 +542,16 @@ def calib_copy(src: torch.Tensor, dst: torch.Tensor):
     if not (src.is_contiguous() and dst.is_contiguous()) or dst.numel() * dst.element_size() < n:
         raise NexusError(EINVAL, "calib_copy: contiguous src, and dst at least as large")
     _check(lib().nexus_calib_copy(_ptr(src), _ptr(dst), n, _stream()), "nexus_calib_copy")
+
+
+def calib_lds_dma(src: torch.Tensor):
+    """Stream src's bytes into LDS with LDS DMA loads (measurement helper: the reference for the
+    memory counters' reading of the attention kernels' loads)."""
+    _on_device(("src", src))
+    n = src.numel() * src.element_size()
+    if not src.is_contiguous() or n == 0 or n % 16384:
+        raise NexusError(EINVAL, "calib_lds_dma: contiguous src of a multiple of 16384 bytes")
+    _check(lib().nexus_calib_lds_dma(_ptr(src), n, _stream()), "nexus_calib_lds_dma")
 
 
 def calib_mfma_bf16(iters: int, sink: torch.Tensor) -> float:
