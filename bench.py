@@ -199,6 +199,22 @@ def run_step(S, events=None):
                 workspace=S["ws"]))
 
 
+def attn_calls(S):
+    """The attention calls of one step, one closure per layer (the calls run_step times)."""
+    from paper_2608_20397_amd import nexus as N
+    wl, cache = S["wl"], S["cache"]
+    nb = len(wl.splice_pos)
+    if nb == 1:
+        return [lambda layer=layer: N.suffix_attn(S["q"][layer], cache, layer, wl.attn_n_past[0],
+                                                  wl.softcap, out=S["out"][layer],
+                                                  workspace=S["ws"])
+                for layer in range(wl.n_layers)]
+    return [lambda layer=layer: N.suffix_attn_varlen(
+        S["q"][layer], [b * wl.n_suffix for b in range(nb)], [wl.n_suffix] * nb,
+        list(wl.attn_n_past), cache, layer, wl.softcap, out=S["out"][layer], workspace=S["ws"])
+        for layer in range(wl.n_layers)]
+
+
 def cpu_baseline(cfg: int, n_kv_sample: int, n_layers: int, n_blocks: int = 0):
     """The fp64 oracle on a bounded sample: the first ``n_layers`` layers' splice + re-anchor
     (all heads) and the attention of ``n_kv_sample`` KV heads' query groups of the first
@@ -733,6 +749,10 @@ def config_summary(S, ms: float, mean: dict, hbm: dict, peaks: dict):
     fl = attn_flops(wl)
     tf = fl / (mean["attn"] * 1e-3) / 1e12
     splice_b, rephase_b = 4 * blk_bytes, 2 * blk_bytes
+    # the step's attention calls replayed back to back from a HIP graph: no host enqueue gaps
+    # (which the per-call events of a short single-layer call include)
+    alone_ms = time_rotating(attn_calls(S), max(3, 10 // wl.n_layers))
+    tf_alone = fl / (alone_ms * 1e-3) / 1e12
     return {
         "workload": f"cfg{wl.cfg}: {wl.name}",
         "dtype": wl.dtype,
@@ -743,6 +763,11 @@ def config_summary(S, ms: float, mean: dict, hbm: dict, peaks: dict):
                  "mean_launch_ms": mean["attn"], "flops_per_launch": fl,
                  "traffic": measured_traffic(wl.cfg),
                  "mfma_busy": measured_mfma_busy(wl.cfg),
+                 "alone": {"mean_launch_ms": alone_ms, "achieved_TFLOPs": tf_alone,
+                           "frac": tf_alone / MFMA_BF16_PEAK_TFLOPS,
+                           "timing": "the step's attention calls back to back in a HIP graph "
+                                     "(operands may stay in the Infinity Cache between calls "
+                                     "of a one-layer config)"},
                  "launches_per_step": wl.n_layers,
                  "call": "nexus_suffix_attn" if nb == 1 else f"nexus_suffix_attn_varlen ({nb} "
                                                               f"suffixes)"},
@@ -885,6 +910,7 @@ def main():
                                "(SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs))"),
             "algorithmic_flops_per_launch": fl_layer,
             "mean_launch_ms": mean["attn"],
+            "alone": summ["attn"]["alone"],
             "frac_of_measured_peak": attn_tflops / peaks["mfma_bf16_TFLOPs"],
         },
         "roofline_hbm": {
