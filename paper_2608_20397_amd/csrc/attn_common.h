@@ -82,10 +82,12 @@ struct AttnPlan {
   int32_t total_rows;
   int32_t any_split;
   size_t ws_bytes;
-  int32_t range_major;                        // 0: units sequence by sequence (first_unit)
+  int32_t range_major;                        // 0: units sequence by sequence (first_unit,
+                                              // sequences in the order of `order`)
   int32_t n_ranges;
   int32_t range_first_unit[kMaxRanges + 1];   // first unit of each key range
-  int32_t order[kMaxSeqs];                    // sequences by decreasing key count
+  int32_t order[kMaxSeqs];                    // range-major: sequences by decreasing key
+                                              // count; else the dispatch order
   int32_t tg_prefix[kMaxSeqs + 1];            // task groups of order[0 .. i - 1]
 };
 
@@ -97,8 +99,10 @@ struct UnitLoc {
 __device__ __forceinline__ UnitLoc locate_unit(const AttnPlan &plan, int unit) {
   UnitLoc loc;
   if (!plan.range_major) {
-    int b = 0;
-    while (b + 1 < plan.n_seqs && unit >= plan.seq[b + 1].first_unit) ++b;
+    // sequences in dispatch order (plan.order): their first units increase along it
+    int i = 0;
+    while (i + 1 < plan.n_seqs && unit >= plan.seq[plan.order[i + 1]].first_unit) ++i;
+    const int b = plan.order[i];
     loc.seq = b;
     loc.w = unit_work(plan.seq[b], unit - plan.seq[b].first_unit);
     return loc;
