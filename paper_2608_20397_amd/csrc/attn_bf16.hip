@@ -448,7 +448,7 @@ struct KernelShape {
 
 KernelShape kernel_shape(const AttnLaunch &p) {
   if (p.head_dim == 128 && !p.v_transposed) return {kQB, 64, 2, kWaves, 0.03};   // LDS DMA
-  if (p.head_dim == 256 && p.v_transposed) return {kQB, 32, 2, kWaves, 0.06};   // LDS DMA
+  if (p.head_dim == 256 && p.v_transposed) return {kQB, 32, 1, kWavesWide, 0.04};   // LDS DMA
   return {kQB, key_tile_for(p.head_dim), p.head_dim >= 256 ? 1 : 2, kWaves,
           0.03 * p.head_dim / 128.0};
 }

@@ -7,6 +7,7 @@ namespace nexus {
 
 constexpr int kMaxSeqs = 32;
 constexpr int kWaves = 4;   // wave tasks per workgroup of the 32-query kernels
+constexpr int kWavesWide = 8;   // wave tasks per workgroup of the head_dim-256 transposed-V kernel
 constexpr int kQB = 32;     // queries per wave task of the 32-query kernels
 constexpr int kMaxSplitKeys = 32768;   // keys one workgroup covers at most (LDS page table)
 
