@@ -51,3 +51,35 @@ def test_random_geometry_parity(i):
     print(tag, flush=True)
     hc = G.host_case_wl(wl, 300 + i)
     _run_full(hc, tag)
+
+
+def _draw_d256(i: int) -> dict:
+    """head_dim 256 with a transposed V (the soft-capped family's kernel): GQA groups 1..8, so
+    that workgroups of 8 wave tasks hold several query blocks and heads or leave slots idle,
+    contexts deep enough for several key splits, the cap on or off, ragged suffixes."""
+    r = np.random.default_rng([20397, 901, i])
+    n_kv = int(r.choice([1, 2, 4]))
+    g = int(r.choice([1, 2, 3, 5, 8]))
+    n_ctx = int(r.integers(0, 3000))
+    block = int(r.integers(1, 300))
+    n_user = int(r.integers(0, 65))
+    n_suffix = int(r.integers(1, block + n_user + 1))
+    kw = dict(head_dim=256, n_kv_heads=n_kv, n_q_heads=g * n_kv, v_layout="transposed",
+              softcap=float(r.choice([0.0, 20.0, 50.0, 50.0])),
+              shuffled_pages=bool(r.integers(0, 2)))
+    return dict(base=5, n_ctx=n_ctx, block=block, n_user=n_user, n_suffix=n_suffix, kw=kw)
+
+
+CASES_D256 = [_draw_d256(i) for i in range(10)]
+
+
+@pytest.mark.parametrize("i", range(len(CASES_D256)))
+def test_random_d256_transposed_parity(i):
+    c = CASES_D256[i]
+    wl = custom_workload(c["base"], c["n_ctx"], c["block"], c["n_user"], c["n_suffix"], **c["kw"])
+    tag = (f"random D256 {i}: Hkv={wl.n_kv_heads} Hq={wl.n_q_heads} ctx {c['n_ctx']} "
+           f"block {c['block']} user {c['n_user']} suffix {c['n_suffix']} cap {wl.softcap} "
+           f"shuffled {wl.shuffled_pages}")
+    print(tag, flush=True)
+    hc = G.host_case_wl(wl, 400 + i)
+    _run_full(hc, tag)
