@@ -471,9 +471,10 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   const int KT = ks.key_tile;
   const int64_t slots = (int64_t)kCUs * ks.wgs_per_cu;
   constexpr int64_t kPieceOverhead = 128;
-  // shortest split in general, and in a launch whose pieces all fit one per CU (a few hundred
-  // queries: latency-bound, where shorter pieces shorten the critical path; measured on the
-  // shallow depths of the depth-adaptive sweep, e.g. 90 queries at 742: 22.8 -> 19.1 us)
+  // shortest split in general, and in a launch whose pieces all fit the resident workgroup slots
+  // at once (a few hundred queries: latency-bound, where shorter pieces shorten the critical
+  // path; measured on the shallow depths of the depth-adaptive sweep, e.g. 90 queries at 742:
+  // 22.8 -> 19.1 us, and on a single layer of 192 queries over 2560 keys: 34.1 -> 32.4 us)
   constexpr int64_t kMinSplitKeys = 512, kMinSplitKeysSmall = 256;
   plan = AttnPlan{};
   plan.n_seqs = p.n_seqs;
@@ -563,7 +564,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
       if (!wk.empty()) max_piece = std::max(max_piece, std::min(skb, wk.back()) + kPieceOverhead);
       total += (seq_keys[b] + (double)pieces * kPieceOverhead) * p.n_kv_heads;
     }
-    if (sk < kMinSplitKeys && ns > 1 && n_pieces > kCUs) continue;
+    if (sk < kMinSplitKeys && ns > 1 && n_pieces > slots) continue;
     if (ws_need > cap) continue;
     const double rounds_full = (double)((n_full + slots - 1) / slots);
     const double est = std::max({rounds_full * (double)(full_len + kPieceOverhead),
