@@ -6,7 +6,8 @@
 //   KV head's group and 32 consecutive queries.  Tasks are ordered query-major, so the 4 waves of
 //   a workgroup need nearly the same key range; the workgroup stages every key tile once in LDS
 //   and all 4 waves read it (the GQA group shares its K/V).  The key axis may be split over
-//   several workgroups; a fixed-order combine kernel then merges the partial (m, l, O).
+//   several workgroups; a fixed-order combine kernel then merges the partials (m, l and O / l
+//   as a scaled fp16 row, store_partial).
 //   blockIdx.x % n_kv_heads selects the KV head, so on the 8-XCD MI355X every workgroup of one
 //   KV head lands on the same XCD and its K/V tiles are shared through that XCD's L2.
 //
@@ -334,6 +335,8 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
 
   // ---- epilogue
   const float l_tot = l + __shfl_xor(l, 32);
+  float part_c = 0.f, part_sc = 0.f;
+  if (uw.n_splits > 1) part_sc = part_scale(row_amax(o), l_tot, part_c);
   if (!active || q0 + j >= sp.len) return;
   const int row = q0 + j;  // within the sequence
   if (uw.n_splits == 1) {
@@ -350,31 +353,23 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
       }
   } else {
     const int64_t prow = ((int64_t)split * sp.len + row) * a.n_q_heads + qhead;
-    float *op = a.ws + sp.ws_off + prow * D;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int gq = 0; gq < 4; ++gq) {
-        const int d0 = 32 * db + 8 * gq + 4 * hh;
-        *reinterpret_cast<float4 *>(op + d0) =
-            make_float4(o[db][4 * gq + 0], o[db][4 * gq + 1], o[db][4 * gq + 2], o[db][4 * gq + 3]);
-      }
-    if (hh == 0) *reinterpret_cast<float2 *>(a.ws + sp.ml_off + prow * 2) = make_float2(m_ref, l_tot);
+    store_partial<NDB, D>(o, part_sc, m_ref, l_tot, part_c, hh, a.ws, sp, prow);
   }
 }
 
-// Fixed-order merge of the split partials: m = max m_s, w_s = 2^(m_s - m),
-// out = sum_s w_s O_s / sum_s w_s l_s.  One thread per 4 output features.
+// Fixed-order merge of the split partials (fp16 rows P_s = O_s / (l_s 2^e_s), records
+// {m_s, l_s, c_s = l_s 2^e_s}): M = max m_s, w_s = 2^(m_s - M),
+// out = sum_s w_s c_s P_s / sum_s w_s l_s.  One thread per 8 output features.
 constexpr int kCombinePre = 8;   // splits whose partials the combine loads up front
 
 template <int D>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a, const AttnPlan plan) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  constexpr int Q4 = D / 4;
-  const int64_t total = (int64_t)plan.total_rows * a.n_q_heads * Q4;
+  constexpr int Q8 = D / 8;
+  const int64_t total = (int64_t)plan.total_rows * a.n_q_heads * Q8;
   if (gid >= total) return;
-  const int d4 = (int)(gid % Q4);
-  const int64_t rh = gid / Q4;
+  const int d8 = (int)(gid % Q8);
+  const int64_t rh = gid / Q8;
   const int head = (int)(rh % a.n_q_heads);
   const int rowg = (int)(rh / a.n_q_heads);
   int b = 0;
@@ -386,52 +381,55 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a, con
   if (n_splits == 1) return;
   const int64_t pstep = (int64_t)sp.len * a.n_q_heads;         // partial rows per split
   const int64_t prow0 = (int64_t)row * a.n_q_heads + head;
+  const f32x4 *rec = reinterpret_cast<const f32x4 *>(a.ws + sp.ml_off);
+  const u32x4 *part = reinterpret_cast<const u32x4 *>(a.ws + sp.ws_off) + d8;
   float mmax = -INFINITY;
   float lsum = 0.f;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+  auto add = [&](const f32x4 &ml, const u32x4 &ov) {
+    const float w = (ml[0] == -INFINITY) ? 0.f : fast_exp2(ml[0] - mmax);
+    lsum += w * ml[1];
+    const float wc = w * ml[2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const f32x2 f = unpack_f16x2(ov[i]);
+      acc[2 * i] += wc * f[0];
+      acc[2 * i + 1] += wc * f[1];
+    }
+  };
   if (n_splits <= kCombinePre) {
-    // every split's (m, l) and O loaded up front (splits past n_splits re-read the last one
+    // every split's record and row loaded up front (splits past n_splits re-read the last one
     // and weigh 0), then merged in split order: one round trip instead of one per split
-    float2 ml[kCombinePre];
-    float4 ov[kCombinePre];
+    f32x4 ml[kCombinePre];
+    u32x4 ov[kCombinePre];
 #pragma unroll
     for (int s = 0; s < kCombinePre; ++s) {
       const int64_t prow = min(s, n_splits - 1) * pstep + prow0;
-      ml[s] = *reinterpret_cast<const float2 *>(a.ws + sp.ml_off + prow * 2);
-      ov[s] = *reinterpret_cast<const float4 *>(a.ws + sp.ws_off + prow * D + 4 * d4);
+      ml[s] = rec[prow];
+      ov[s] = part[prow * Q8];
     }
 #pragma unroll
     for (int s = 0; s < kCombinePre; ++s)
-      if (s < n_splits) mmax = fmaxf(mmax, ml[s].x);
+      if (s < n_splits) mmax = fmaxf(mmax, ml[s][0]);
 #pragma unroll
     for (int s = 0; s < kCombinePre; ++s) {
       if (s >= n_splits) break;
-      const float w = (ml[s].x == -INFINITY) ? 0.f : fast_exp2(ml[s].x - mmax);
-      lsum += w * ml[s].y;
-      acc.x += w * ov[s].x;
-      acc.y += w * ov[s].y;
-      acc.z += w * ov[s].z;
-      acc.w += w * ov[s].w;
+      add(ml[s], ov[s]);
     }
   } else {
-    for (int s = 0; s < n_splits; ++s)
-      mmax = fmaxf(mmax, a.ws[sp.ml_off + (s * pstep + prow0) * 2]);
+    for (int s = 0; s < n_splits; ++s) mmax = fmaxf(mmax, rec[s * pstep + prow0][0]);
     for (int s = 0; s < n_splits; ++s) {
       const int64_t prow = s * pstep + prow0;
-      const float2 ml = *reinterpret_cast<const float2 *>(a.ws + sp.ml_off + prow * 2);
-      const float w = (ml.x == -INFINITY) ? 0.f : fast_exp2(ml.x - mmax);
-      lsum += w * ml.y;
-      const float4 ov = *reinterpret_cast<const float4 *>(a.ws + sp.ws_off + prow * D + 4 * d4);
-      acc.x += w * ov.x;
-      acc.y += w * ov.y;
-      acc.z += w * ov.z;
-      acc.w += w * ov.w;
+      add(rec[prow], part[prow * Q8]);
     }
   }
   const float inv = 1.0f / lsum;
-  uint16_t *orow = a.out + ((int64_t)(sp.q_start + row) * a.n_q_heads + head) * D + 4 * d4;
-  *reinterpret_cast<uint2 *>(orow) =
-      make_uint2(pack_bf16x2(acc.x * inv, acc.y * inv), pack_bf16x2(acc.z * inv, acc.w * inv));
+  uint16_t *orow = a.out + ((int64_t)(sp.q_start + row) * a.n_q_heads + head) * D + 8 * d8;
+  *reinterpret_cast<u32x4 *>(orow) =
+      u32x4{pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv),
+            pack_bf16x2(acc[4] * inv, acc[5] * inv), pack_bf16x2(acc[6] * inv, acc[7] * inv)};
 }
 
 namespace {
@@ -461,8 +459,8 @@ constexpr int kCUs = 256;
 // the resident workgroup slots (the longest piece of work, the total work spread over the slots,
 // and the rounds that the near-full-length pieces need: uniform suffix shapes are decided by the
 // the latter, causal prefills by the former two) at the kernel's measured time per key of one
-// workgroup (KernelShape), plus, when keys are split, the combine: writing and reading the fp32
-// partials at about 4 TB/s and one more launch.  A piece's work is its keys plus a fixed 128 for
+// workgroup (KernelShape), plus, when keys are split, the combine: writing and reading the
+// partials (fp16 rows and their records) at about 4 TB/s and one more launch.  A piece's work is its keys plus a fixed 128 for
 // its prologue and epilogue.
 bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   if (p.n_seqs < 1 || p.n_seqs > kMaxSeqs) return false;
@@ -519,9 +517,10 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   double best_cost = 1e300;
   bool found = false;
   const double cap = p.ws_cap == SIZE_MAX ? 1e300 : (double)p.ws_cap;
-  // workspace bytes of a sequence whose rows keep `n` partials each (none for one split)
+  // workspace bytes of a sequence whose rows keep `n` partials each (none for one split): an
+  // fp16 row and a 16-byte record per partial
   auto part_bytes = [&](const AttnSeq &s, int64_t n) {
-    return n > 1 ? 4.0 * (double)n * s.len * p.n_q_heads * (p.head_dim + 2) : 0.0;
+    return n > 1 ? (double)n * s.len * p.n_q_heads * (2.0 * p.head_dim + 16.0) : 0.0;
   };
   for (int ns = 1; ns <= kMaxRanges; ++ns) {
     int64_t sk = (max_keys + ns - 1) / ns;
@@ -539,8 +538,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
       max_splits = std::max(max_splits, nsb);
       ws_need += part_bytes(s, nsb);
       if (nsb > 1)
-        combine_bytes += 8.0 * nsb * s.len * p.n_q_heads * (p.head_dim + 2) +
-                         2.0 * s.len * p.n_q_heads * p.head_dim;
+        combine_bytes += 2.0 * part_bytes(s, nsb) + 2.0 * s.len * p.n_q_heads * p.head_dim;
       // piece j of a task group is non-empty when its keys exceed j * skb, and counts as
       // full-length for the rounds when it holds at least half the split length.  Suffix-like
       // sequences (all task groups within 10% of the same keys) take the closed form.
@@ -610,7 +608,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
         if (part_bytes(s, std::max(cut_count(ns_a), cut_count(ns_b))) > cap) continue;
         const int64_t rounds_a = (n_a * ns_a + slots_h - 1) / slots_h;
         const double est = (double)rounds_a * (la + kPieceOverhead) + (double)(lb + kPieceOverhead);
-        const double comb = 8.0 * rows_heads * (p.head_dim + 2) *
+        const double comb = 2.0 * rows_heads * (2.0 * p.head_dim + 16.0) *
                                 (double)(n_a * ns_a + n_b * ns_b) / (double)n_tg +
                             2.0 * rows_heads * p.head_dim;
         const double cost = est * ks.us_per_key + comb / 4.0e6 + 8.0;
@@ -625,7 +623,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   }
 
   int32_t unit = 0, rows = 0;
-  int64_t ws_floats = 0;
+  int64_t ws_bytes = 0;
   int32_t seq_units[kMaxSeqs];
   for (int b = 0; b < p.n_seqs; ++b) {
     const AttnSeq &s = p.seqs[b];
@@ -670,15 +668,15 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
     rows += s.len;
     if (sp.max_splits > 1) {
       plan.any_split = 1;
-      sp.ws_off = ws_floats;
-      ws_floats += (int64_t)sp.max_splits * s.len * p.n_q_heads * p.head_dim;
-      sp.ml_off = ws_floats;
-      ws_floats += (int64_t)sp.max_splits * s.len * p.n_q_heads * 2;
+      sp.ws_off = ws_bytes;
+      ws_bytes += ((int64_t)sp.max_splits * s.len * p.n_q_heads * p.head_dim * 2 + 15) / 16 * 16;
+      sp.ml_off = ws_bytes;
+      ws_bytes += (int64_t)sp.max_splits * s.len * p.n_q_heads * 16;
     }
   }
   plan.units_per_head = unit;
   plan.total_rows = rows;
-  plan.ws_bytes = (size_t)ws_floats * sizeof(float);
+  plan.ws_bytes = (size_t)ws_bytes;
   if (!range_major) {
     // dispatch order: suffix-like sequences first (uniform units), then causal prefills, whose
     // longest-first order ends the launch on their short diagonal groups
@@ -763,7 +761,7 @@ hipError_t launch_attention(const AttnLaunch &p, hipStream_t stream) {
   args.kc = (const uint16_t *)p.cache_k + (int64_t)p.layer * layer_elems;
   args.vc = (const uint16_t *)p.cache_v + (int64_t)p.layer * layer_elems;
   args.map = p.map;
-  args.ws = (float *)p.workspace;
+  args.ws = (char *)p.workspace;
   args.n_q_heads = p.n_q_heads;
   args.n_kv_heads = p.n_kv_heads;
   args.group = p.n_q_heads / p.n_kv_heads;
@@ -797,7 +795,7 @@ hipError_t launch_attention(const AttnLaunch &p, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (plan.any_split) {
-    const int64_t total = (int64_t)plan.total_rows * p.n_q_heads * (p.head_dim / 4);
+    const int64_t total = (int64_t)plan.total_rows * p.n_q_heads * (p.head_dim / 8);
     const uint32_t blocks = (uint32_t)((total + 255) / 256);
     switch (p.head_dim) {
       case 64: hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(blocks), dim3(256), 0, stream, args, plan); break;

@@ -412,6 +412,8 @@ __global__ __launch_bounds__(64 * kWavesWide, 1) void attn_bf16_d256_vt_kernel(
 
   // ---- epilogue
   const float l_tot = sum_halves(l);
+  float part_c = 0.f, part_sc = 0.f;
+  if (uw.n_splits > 1) part_sc = part_scale(row_amax(o), l_tot, part_c);
   if (!active || q0 + j >= sp.len) return;
   const int row = q0 + j;
   if (uw.n_splits == 1) {
@@ -428,16 +430,7 @@ __global__ __launch_bounds__(64 * kWavesWide, 1) void attn_bf16_d256_vt_kernel(
       }
   } else {
     const int64_t prow = ((int64_t)uw.split * sp.len + row) * a.n_q_heads + qhead;
-    float *op = a.ws + sp.ws_off + prow * D;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int gq = 0; gq < 4; ++gq) {
-        const int d0 = 32 * db + 8 * gq + 4 * hh;
-        *reinterpret_cast<f32x4 *>(op + d0) =
-            f32x4{o[db][4 * gq + 0], o[db][4 * gq + 1], o[db][4 * gq + 2], o[db][4 * gq + 3]};
-      }
-    if (hh == 0) *reinterpret_cast<f32x2 *>(a.ws + sp.ml_off + prow * 2) = f32x2{m_ref, l_tot};
+    store_partial<NDB, D>(o, part_sc, m_ref, l_tot, part_c, hh, a.ws, sp, prow);
   }
 }
 

@@ -22,8 +22,8 @@ struct SeqPlan {
   int32_t n_splits;
   int32_t split_keys;  // keys per split, a multiple of the key tile
   int32_t longest_first;  // dispatch task groups last-first (causal prefill: n_past < len)
-  int64_t ws_off;      // float offset of the partial O of this sequence in the workspace
-  int64_t ml_off;      // float offset of its (m, l) pairs
+  int64_t ws_off;      // byte offset of the fp16 partial rows of this sequence in the workspace
+  int64_t ml_off;      // byte offset of their {m, l, l 2^e, 0} records (16-byte aligned)
   // Two split classes: the first n_tg_a task groups in dispatch order take n_splits splits of
   // split_keys keys, the others n_splits_b splits of split_keys_b (a finer cut that fills the
   // last round of workgroups).  One class: n_tg_a = all groups, class b equal to class a.
@@ -138,7 +138,7 @@ struct AttnArgs {
   const uint16_t *kc;   // layer base of the K cache
   const uint16_t *vc;   // layer base of the V cache
   const int32_t *map;
-  float *ws;
+  char *ws;             // split partials: fp16 rows at SeqPlan::ws_off, records at ml_off
   int32_t n_q_heads, n_kv_heads, group, n_phys_pages;
   float scale_log2;     // scale * log2(e)
   float cap_in;         // scale / softcap
@@ -157,6 +157,54 @@ __device__ __forceinline__ float tanh_fast(float x) {
 // r = 0, the cap itself; underflowing to 0 gives r = 1).
 __device__ __forceinline__ float cap_r(float s, float cap_k) {
   return __builtin_amdgcn_rcpf(fast_exp2(s * cap_k) + 1.0f);
+}
+
+// Split-K partial of one output row (query, head) of the bf16 kernels, from the lane pair
+// (j, j + 32) that holds the row: its O / l as fp16, scaled by 2^-e so that the row's largest
+// magnitude lies in [2^14, 2^15), and the record {m, l, l 2^e, 0} that the combine weighs it
+// with.  fp16 keeps 11 significant bits over the scaled range (the final output is bf16, 8
+// bits); the power-of-two scale keeps any finite V in range and costs no rounding.
+// part_scale: the factor that maps O to the stored values, and l 2^e in `c`.  Every lane of the
+// wave calls it (cross-lane maximum); `amax` is the lane's largest |O| over its features.
+__device__ __forceinline__ float part_scale(float amax, float l_tot, float &c) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(amax), __float_as_uint(amax),
+                                                  false, false);
+  amax = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+  const float rmax = amax * inv;
+  int e = 0;
+  if (rmax > 0.f && rmax <= 3.0e38f)
+    e = min(max((int)((__float_as_uint(rmax) >> 23) & 0xff) - 127 - 14, -100), 100);
+  c = l_tot * __uint_as_float((uint32_t)(127 + e) << 23);
+  return inv * __uint_as_float((uint32_t)(127 - e) << 23);
+}
+template <int NDB>
+__device__ __forceinline__ float row_amax(const f32x16 (&o)[NDB]) {
+  float m = 0.f;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) m = fmaxf(m, fabsf(o[db][v]));
+  return m;
+}
+// Stores the lane's features of the row: feature 32 db + 8 gq + 4 hh + i holds o[db][4 gq + i]
+// (the 32x32 MFMA accumulator layout of O^T), and the record from lane half 0.
+template <int NDB, int D>
+__device__ __forceinline__ void store_partial(const f32x16 (&o)[NDB], float sc, float m_ref,
+                                              float l_tot, float c, int hh, char *ws,
+                                              const SeqPlan &sp, int64_t prow) {
+  uint16_t *op = reinterpret_cast<uint16_t *>(ws + sp.ws_off) + prow * D;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      const int d0 = 32 * db + 8 * gq + 4 * hh;
+      *reinterpret_cast<u32x2 *>(op + d0) =
+          u32x2{pack_f16x2(o[db][4 * gq + 0] * sc, o[db][4 * gq + 1] * sc),
+                pack_f16x2(o[db][4 * gq + 2] * sc, o[db][4 * gq + 3] * sc)};
+    }
+  if (hh == 0)
+    *reinterpret_cast<f32x4 *>(ws + sp.ml_off + prow * 16) = f32x4{m_ref, l_tot, c, 0.f};
 }
 
 // key index within a 16-key group -> its position in the V^T tile (swap bits 2 and 3)

@@ -167,6 +167,33 @@ def test_rerun_and_page_table_invariance():
     assert torch.equal(o1.view(torch.int16), o3.view(torch.int16))
 
 
+@pytest.mark.parametrize("base,kw", [
+    (2, dict(n_ctx=6000, block_len=64, n_user=0, n_suffix=64)),                 # head_dim 128
+    (5, dict(n_ctx=5000, block_len=64, n_user=0, n_suffix=64)),                 # 256, V^T, cap
+    (2, dict(n_ctx=3000, block_len=64, n_user=0, n_suffix=40, head_dim=64, n_q_heads=16,
+             n_kv_heads=4)),                                                    # 64 (generic)
+])
+def test_split_partials_power_of_two_scale_equivariance(base, kw):
+    """Split partials hold O / l as fp16 under a per-row power-of-two scale: V scaled by 2^20
+    (values beyond fp16's range) or 2^-20 (below its normal range) gives the unscaled launch's
+    output scaled by the same power of two, bit for bit, through a split plan."""
+    outs = {}
+    for e in (0, 20, -20):
+        wl = custom_workload(base, **kw)
+        wl = dataclasses.replace(wl, v_scale=wl.v_scale * 2.0 ** e)
+        hc = G.host_case_wl(wl, 555)
+        cache = gpu_build_cache(hc)
+        if e == 0:
+            assert N.suffix_attn_workspace_bytes(cache, wl.n_suffix, wl.n_q_heads,
+                                                 wl.attn_n_past[0]) > 0, "no split plan"
+        outs[e] = gpu_attention(hc, cache).out[0]
+    torch.cuda.synchronize()
+    ref = outs[0].float()
+    assert torch.isfinite(ref).all() and ref.abs().max() > 0
+    for e in (20, -20):
+        assert torch.equal(outs[e].float(), ref * 2.0 ** e), e
+
+
 def test_transposed_equals_rowmajor_values():
     """The same logical V in both layouts gives outputs within tolerance of each other."""
     wl_t = custom_workload(5, n_ctx=1000, block_len=200, n_user=0, n_suffix=100)

@@ -2,10 +2,11 @@
 nexus_suffix_attn (caller workspace), through the C ABI.
 
 Calls in a row on one GPU share the array: a long suffix whose workspace plan does not fit the
-array (Qwen2.5-14B shapes, 1088 queries at depth 16384: a capped plan, so within the bf16
+array (Qwen2.5-14B shapes, 2048 queries at depth 16384: a capped plan, so within the bf16
 attention tolerance of the workspace call), then a shorter one whose plan fits (192 queries at
 2432: bit-identical), then head_dim 256 with a transposed V and a soft cap (256 queries at 1792:
-bit-identical), and a suffix no plan fits into the array (refused, nothing written).
+bit-identical), and a suffix no plan fits into the array (refused, nothing written).  A split
+partial takes 2 * head_dim + 16 bytes per row and head (fp16 row, fp32 record).
 """
 
 import math
@@ -41,9 +42,10 @@ def _rel(a, b):
 
 def test_noalloc_matches_workspace_call_twice_then_smaller():
     limit = 64 << 20
-    # 1: config 3's attention geometry; its workspace plan needs more than the array holds
-    cache, q = _case(70, 40, 8, 128, 16384, 1088)
-    need = N.suffix_attn_workspace_bytes(cache, 1088, 40, 16384)
+    # 1: Qwen2.5-14B attention shapes, 2048 queries at depth 16384; its workspace plan needs
+    # more than the array holds
+    cache, q = _case(70, 40, 8, 128, 16384, 2048)
+    need = N.suffix_attn_workspace_bytes(cache, 2048, 40, 16384)
     assert need > limit
     ref = N.suffix_attn(q, cache, 0, 16384)
     got = torch.full_like(q, float("nan"))
@@ -51,7 +53,7 @@ def test_noalloc_matches_workspace_call_twice_then_smaller():
     torch.cuda.synchronize()
     assert torch.isfinite(got.float()).all()
     ma, rr = _rel(got, ref)
-    print(f"noalloc 1088 @ 16384 (capped plan): max-abs {ma:.3e} rel-RMS {rr:.3e}", flush=True)
+    print(f"noalloc 2048 @ 16384 (capped plan): max-abs {ma:.3e} rel-RMS {rr:.3e}", flush=True)
     assert ma <= MAX_ABS and rr <= REL_RMS
     # 2: a smaller call right after: the plan fits, so the result is bit-identical
     cache2, q2 = _case(71, 40, 8, 128, 2432, 192)
@@ -79,10 +81,10 @@ def test_noalloc_head_dim_256_transposed_softcap_is_bit_identical():
 
 
 def test_noalloc_refuses_a_suffix_no_plan_fits():
-    # 2048 queries x 40 heads over 34816 keys: at least two splits (a split covers <= 32768
-    # keys), whose partials (2 x 2048 x 40 x 130 x 4 bytes) exceed the array
-    cache, q = _case(73, 40, 8, 128, 32768, 2048)
-    assert 2 * 2048 * 40 * 130 * 4 > 64 << 20
+    # 4096 queries x 40 heads over 36864 keys: at least two splits (a split covers <= 32768
+    # keys), whose partials (2 x 4096 x 40 x (2 x 128 + 16) bytes) exceed the array
+    cache, q = _case(73, 40, 8, 128, 32768, 4096)
+    assert 2 * 4096 * 40 * (2 * 128 + 16) > 64 << 20
     out = torch.full_like(q, 7.0)
     with pytest.raises(N.NexusError) as e:
         N.suffix_attn_noalloc(q, cache, 0, 32768, out=out)
