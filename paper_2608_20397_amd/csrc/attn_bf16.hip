@@ -460,7 +460,7 @@ constexpr int kCUs = 256;
 // and the rounds that the near-full-length pieces need: uniform suffix shapes are decided by the
 // the latter, causal prefills by the former two) at the kernel's measured time per key of one
 // workgroup (KernelShape), plus, when keys are split, the combine: writing and reading the
-// partials (fp16 rows and their records) at about 4 TB/s and one more launch.  A piece's work is its keys plus a fixed 128 for
+// partials (priced as fp32 rows, split_cost_bytes) at about 4 TB/s and one more launch.  A piece's work is its keys plus a fixed 128 for
 // its prologue and epilogue.
 bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   if (p.n_seqs < 1 || p.n_seqs > kMaxSeqs) return false;
@@ -522,6 +522,16 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   auto part_bytes = [&](const AttnSeq &s, int64_t n) {
     return n > 1 ? (double)n * s.len * p.n_q_heads * (2.0 * p.head_dim + 16.0) : 0.0;
   };
+  // the split term of the cost: 8 (D + 2) bytes per partial row, i.e. its write and read as
+  // fp32 O and (m, l).  The partials are stored at about half that (fp16 rows), but the term was
+  // calibrated with these bytes, and it also stands for the per-unit costs of a split that the
+  // estimate leaves out (more workgroups and prologues, empty units of causal groups): pricing
+  // it at the stored bytes chose more splits and ran slower (one launch of a 2048-token prefill
+  // and a 576-token suffix: 77 -> 121 us per layer; 123 queries at depth 512 with a 512-token
+  // prefill: 25.6 -> 31.6 us), with configs 2 and 4 unchanged.
+  auto split_cost_bytes = [&](const AttnSeq &s, int64_t n) {
+    return n > 1 ? 8.0 * (double)n * s.len * p.n_q_heads * (p.head_dim + 2) : 0.0;
+  };
   for (int ns = 1; ns <= kMaxRanges; ++ns) {
     int64_t sk = (max_keys + ns - 1) / ns;
     sk = (sk + KT - 1) / KT * KT;
@@ -538,7 +548,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
       max_splits = std::max(max_splits, nsb);
       ws_need += part_bytes(s, nsb);
       if (nsb > 1)
-        combine_bytes += 2.0 * part_bytes(s, nsb) + 2.0 * s.len * p.n_q_heads * p.head_dim;
+        combine_bytes += split_cost_bytes(s, nsb) + 2.0 * s.len * p.n_q_heads * p.head_dim;
       // piece j of a task group is non-empty when its keys exceed j * skb, and counts as
       // full-length for the rounds when it holds at least half the split length.  Suffix-like
       // sequences (all task groups within 10% of the same keys) take the closed form.
@@ -608,7 +618,7 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
         if (part_bytes(s, std::max(cut_count(ns_a), cut_count(ns_b))) > cap) continue;
         const int64_t rounds_a = (n_a * ns_a + slots_h - 1) / slots_h;
         const double est = (double)rounds_a * (la + kPieceOverhead) + (double)(lb + kPieceOverhead);
-        const double comb = 2.0 * rows_heads * (2.0 * p.head_dim + 16.0) *
+        const double comb = 8.0 * rows_heads * (p.head_dim + 2) *
                                 (double)(n_a * ns_a + n_b * ns_b) / (double)n_tg +
                             2.0 * rows_heads * p.head_dim;
         const double cost = est * ks.us_per_key + comb / 4.0e6 + 8.0;
