@@ -359,17 +359,18 @@ __global__ __launch_bounds__(256, (D >= 256 ? 1 : 2)) void attn_bf16_kernel(cons
 
 // Fixed-order merge of the split partials (fp16 rows P_s = O_s / (l_s 2^e_s), records
 // {m_s, l_s, c_s = l_s 2^e_s}): M = max m_s, w_s = 2^(m_s - M),
-// out = sum_s w_s c_s P_s / sum_s w_s l_s.  One thread per 8 output features.
+// out = sum_s w_s c_s P_s / sum_s w_s l_s.  One thread per 16 output features (two 16-byte
+// partial loads per split), which puts config 3's merge in one round of resident workgroups.
 constexpr int kCombinePre = 8;   // splits whose partials the combine loads up front
 
 template <int D>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a, const AttnPlan plan) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  constexpr int Q8 = D / 8;
-  const int64_t total = (int64_t)plan.total_rows * a.n_q_heads * Q8;
+  constexpr int Q8 = D / 8, Q16 = D / 16;
+  const int64_t total = (int64_t)plan.total_rows * a.n_q_heads * Q16;
   if (gid >= total) return;
-  const int d8 = (int)(gid % Q8);
-  const int64_t rh = gid / Q8;
+  const int d8 = 2 * (int)(gid % Q16);
+  const int64_t rh = gid / Q16;
   const int head = (int)(rh % a.n_q_heads);
   const int rowg = (int)(rh / a.n_q_heads);
   int b = 0;
@@ -385,10 +386,10 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a, con
   const u32x4 *part = reinterpret_cast<const u32x4 *>(a.ws + sp.ws_off) + d8;
   float mmax = -INFINITY;
   float lsum = 0.f;
-  float acc[8];
+  float acc[16];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-  auto add = [&](const f32x4 &ml, const u32x4 &ov) {
+  for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+  auto add = [&](const f32x4 &ml, const u32x4 &ov, const u32x4 &ov2) {
     const float w = (ml[0] == -INFINITY) ? 0.f : fast_exp2(ml[0] - mmax);
     lsum += w * ml[1];
     const float wc = w * ml[2];
@@ -397,18 +398,24 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a, con
       const f32x2 f = unpack_f16x2(ov[i]);
       acc[2 * i] += wc * f[0];
       acc[2 * i + 1] += wc * f[1];
+      const f32x2 g = unpack_f16x2(ov2[i]);
+      acc[8 + 2 * i] += wc * g[0];
+      acc[8 + 2 * i + 1] += wc * g[1];
     }
   };
   if (n_splits <= kCombinePre) {
-    // every split's record and row loaded up front (splits past n_splits re-read the last one
-    // and weigh 0), then merged in split order: one round trip instead of one per split
+    // every split's record and row loaded up front, then merged in split order: one round
+    // trip instead of one per split
     f32x4 ml[kCombinePre];
-    u32x4 ov[kCombinePre];
+    u32x4 ov[kCombinePre], ov2[kCombinePre];
 #pragma unroll
     for (int s = 0; s < kCombinePre; ++s) {
-      const int64_t prow = min(s, n_splits - 1) * pstep + prow0;
-      ml[s] = rec[prow];
-      ov[s] = part[prow * Q8];
+      if (s < n_splits) {
+        const int64_t prow = s * pstep + prow0;
+        ml[s] = rec[prow];
+        ov[s] = part[prow * Q8];
+        ov2[s] = part[prow * Q8 + 1];
+      }
     }
 #pragma unroll
     for (int s = 0; s < kCombinePre; ++s)
@@ -416,13 +423,13 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a, con
 #pragma unroll
     for (int s = 0; s < kCombinePre; ++s) {
       if (s >= n_splits) break;
-      add(ml[s], ov[s]);
+      add(ml[s], ov[s], ov2[s]);
     }
   } else {
     for (int s = 0; s < n_splits; ++s) mmax = fmaxf(mmax, rec[s * pstep + prow0][0]);
     for (int s = 0; s < n_splits; ++s) {
       const int64_t prow = s * pstep + prow0;
-      add(rec[prow], part[prow * Q8]);
+      add(rec[prow], part[prow * Q8], part[prow * Q8 + 1]);
     }
   }
   const float inv = 1.0f / lsum;
@@ -430,6 +437,9 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a, con
   *reinterpret_cast<u32x4 *>(orow) =
       u32x4{pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv),
             pack_bf16x2(acc[4] * inv, acc[5] * inv), pack_bf16x2(acc[6] * inv, acc[7] * inv)};
+  *reinterpret_cast<u32x4 *>(orow + 8) =
+      u32x4{pack_bf16x2(acc[8] * inv, acc[9] * inv), pack_bf16x2(acc[10] * inv, acc[11] * inv),
+            pack_bf16x2(acc[12] * inv, acc[13] * inv), pack_bf16x2(acc[14] * inv, acc[15] * inv)};
 }
 
 namespace {
@@ -805,7 +815,7 @@ hipError_t launch_attention(const AttnLaunch &p, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (plan.any_split) {
-    const int64_t total = (int64_t)plan.total_rows * p.n_q_heads * (p.head_dim / 8);
+    const int64_t total = (int64_t)plan.total_rows * p.n_q_heads * (p.head_dim / 16);
     const uint32_t blocks = (uint32_t)((total + 255) / 256);
     switch (p.head_dim) {
       case 64: hipLaunchKernelGGL(attn_combine_kernel<64>, dim3(blocks), dim3(256), 0, stream, args, plan); break;
