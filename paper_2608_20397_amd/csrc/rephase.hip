@@ -2,8 +2,9 @@
 // by delta * theta_i, theta_i = base^(-2i/D), delta = splice position - compile anchor
 // (the inverse of the drift of eq. (drift)).  In place; V is never touched.
 //
-// HBM-bound: each workgroup forms the D/2 angles once in fp64 (reduced modulo 2*pi in fp64) and
-// keeps their cosine and sine in LDS as fp32 head + tail pairs (c = c_hi + c_lo to about 2^-48);
+// HBM-bound: the D/2 angles are formed in fp64 (reduced modulo 2*pi in fp64), their cosine and
+// sine kept as fp32 head + tail pairs (c = c_hi + c_lo to about 2^-48) in LDS: for head_dim <= 256
+// formed on the host and passed with the launch (HOST_TAB), otherwise by each workgroup;
 // each thread owns a fixed group of feature pairs, holds their cos/sin in registers and streams
 // rows with 16-byte non-temporal loads and stores.  The rotation x c - y s is evaluated in fp32
 // with the product y s_hi split exactly by an FMA (Dekker's two-product) and the tail terms
@@ -22,12 +23,12 @@ namespace nexus {
 // blocks and the slots of a partial first or last page that hold no token of the range are
 // skipped.  A workgroup covers kBatch passes of 256 / tpr rows; its loads are issued before the
 // angle table is formed, so the fp64 angles are computed while they are in flight.
-template <typename T, bool INTERLEAVED>
+template <typename T, bool INTERLEAVED, bool HOST_TAB>
 __global__ __launch_bounds__(256) void rephase_kernel(
     T *__restrict__ k, const int32_t *__restrict__ map, int64_t offset, int64_t first_page,
     uint32_t n_rows, uint32_t tpr_shift, FastDiv div_heads, FastDiv div_pages, uint32_t n_heads,
     uint32_t n_range_pages, uint32_t n_tokens, uint32_t n_phys_pages, int32_t head_dim,
-    int64_t delta, double base) {
+    int64_t delta, double base, const RopeTab tab) {
   constexpr int N = Pack<T>::N;
   constexpr int kBatch = 2;
   __shared__ float cs_tab[4][kMaxPairs];   // cos head, cos tail, sin head, sin tail
@@ -67,8 +68,14 @@ __global__ __launch_bounds__(256) void rephase_kernel(
   const uint32_t stride = gridDim.x * per_wg;
   uint32_t wb = blockIdx.x * per_wg;
   issue(wb + sub);
-  for (int i = threadIdx.x; i < head_dim / 2; i += blockDim.x)
-    pair_cs(delta, base, i, head_dim, cs_tab[0][i], cs_tab[1][i], cs_tab[2][i], cs_tab[3][i]);
+  for (int i = threadIdx.x; i < head_dim / 2; i += blockDim.x) {
+    if constexpr (HOST_TAB) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) cs_tab[q][i] = tab.v[q][i];
+    } else {
+      pair_cs(delta, base, i, head_dim, cs_tab[0][i], cs_tab[1][i], cs_tab[2][i], cs_tab[3][i]);
+    }
+  }
   // LDS-only barrier: the row loads above stay in flight
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
@@ -136,18 +143,27 @@ hipError_t launch_rephase(const RephaseLaunch &p, hipStream_t stream) {
   if (blocks < 1) blocks = 1;
   const FastDiv dh = make_fastdiv((uint32_t)p.n_heads);
   const FastDiv dp = make_fastdiv((uint32_t)n_pp);
-#define NEXUS_REPHASE(T, IL)                                                                      \
-  hipLaunchKernelGGL((rephase_kernel<T, IL>), dim3((uint32_t)blocks), dim3(256), 0, stream,      \
+  const bool host_tab = p.head_dim / 2 <= kTabPairs;
+  RopeTab tab{};
+  if (host_tab) rope_tab_host(p.delta, p.rope_base, p.head_dim, tab);
+#define NEXUS_REPHASE(T, IL, HT)                                                                  \
+  hipLaunchKernelGGL((rephase_kernel<T, IL, HT>), dim3((uint32_t)blocks), dim3(256), 0, stream,  \
                      (T *)p.k, p.map, p.offset, first_page, (uint32_t)rows, shift, dh, dp,        \
                      (uint32_t)p.n_heads, (uint32_t)n_pp, (uint32_t)p.n_tokens,                   \
-                     (uint32_t)p.n_phys_pages, p.head_dim, p.delta, p.rope_base)
+                     (uint32_t)p.n_phys_pages, p.head_dim, p.delta, p.rope_base, tab)
+#define NEXUS_REPHASE_T(T, IL)                                                                    \
+  do {                                                                                            \
+    if (host_tab) NEXUS_REPHASE(T, IL, true);                                                     \
+    else NEXUS_REPHASE(T, IL, false);                                                             \
+  } while (0)
   if (p.dtype_bytes == 2) {
-    if (p.interleaved) NEXUS_REPHASE(uint16_t, true);
-    else NEXUS_REPHASE(uint16_t, false);
+    if (p.interleaved) NEXUS_REPHASE_T(uint16_t, true);
+    else NEXUS_REPHASE_T(uint16_t, false);
   } else {
-    if (p.interleaved) NEXUS_REPHASE(uint32_t, true);
-    else NEXUS_REPHASE(uint32_t, false);
+    if (p.interleaved) NEXUS_REPHASE_T(uint32_t, true);
+    else NEXUS_REPHASE_T(uint32_t, false);
   }
+#undef NEXUS_REPHASE_T
 #undef NEXUS_REPHASE
   return hipGetLastError();
 }

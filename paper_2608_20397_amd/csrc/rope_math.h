@@ -4,6 +4,8 @@
 
 #include "device_common.h"
 
+#include <cmath>
+
 namespace nexus {
 
 constexpr double kTwoPiHi = 6.283185307179586232;       // fp64(2*pi)
@@ -76,6 +78,29 @@ __device__ __forceinline__ void rotate(float *a, float *b, const float *ch, cons
     const float xa = a[e], xb = b[e];
     a[e] = rot_dot(xa, xb, ch[e], cl[e], sh[e], sl[e]);      // xa c - xb s
     b[e] = rot_dot(xb, -xa, ch[e], cl[e], sh[e], sl[e]);     // xb c + xa s
+  }
+}
+
+// cos / sin head and tail of every pair of one rotation (angle delta * theta_i for all rows),
+// formed on the host by the same steps as pair_angle / pair_cs and passed to a kernel by value:
+// the fp64 angle code then stays out of the kernel (with it, the re-anchor needs 117 registers
+// and its workgroups spend their start on the angles; without, 68).
+constexpr int kTabPairs = 128;   // head_dim <= 256
+struct RopeTab {
+  float v[4][kTabPairs];         // cos head, cos tail, sin head, sin tail
+};
+inline void rope_tab_host(int64_t delta, double base, int head_dim, RopeTab &t) {
+  for (int i = 0; i < head_dim / 2 && i < kTabPairs; ++i) {
+    const double theta = std::pow(base, -2.0 * (double)i / (double)head_dim);
+    const double ang = (double)delta * theta;
+    const double k = std::rint(ang / kTwoPiHi);
+    double r = std::fma(-k, kTwoPiHi, ang);
+    r = std::fma(-k, kTwoPiLo, r);
+    const double c = std::cos(r), s = std::sin(r);
+    t.v[0][i] = (float)c;
+    t.v[1][i] = (float)(c - (double)t.v[0][i]);
+    t.v[2][i] = (float)s;
+    t.v[3][i] = (float)(s - (double)t.v[2][i]);
   }
 }
 

@@ -9,9 +9,10 @@
 //     row to logical slot offset + j.
 // A workgroup covers kTileTokens tokens of one layer, all heads: its source rows are one
 // contiguous run of the block.  Each thread issues the loads of its first kBatch items, then the
-// workgroup forms, in fp64, the cosine and sine of every (token, pair) angle it needs (one angle
-// per pair when the rotation is the same for every token) and keeps them in LDS as fp32 head +
-// tail pairs while those loads are in flight; then the threads rotate and write their items.
+// workgroup puts the cosine and sine of every (token, pair) angle it needs in LDS as fp32 head +
+// tail pairs while those loads are in flight: with one rotation for every token, the host's
+// table of the launch (the one the re-anchor uses, so both give the same bits), per token formed
+// in fp64 by the workgroup; then the threads rotate and write their items.
 // HBM-bound.
 #include "launch.h"
 #include "rope_math.h"
@@ -25,8 +26,9 @@ namespace {
 // and rope-append 81 us, against 80 and 87 us with 8 tokens and two items per thread, and 84
 // and 91 us with 8 tokens x 16 layers per workgroup)
 constexpr int kTileTokens = 4;        // tokens per workgroup
-constexpr int kMaxPairsTab = 128;     // head_dim <= 256
+constexpr int kMaxPairsTab = kTabPairs;   // head_dim <= 256
 constexpr int kBatch = 1;             // items per thread whose loads are in flight together
+constexpr int kOccCapFloats = 9500;   // LDS reserve: 40 KB per workgroup with the table, 4 per CU
 
 }  // namespace
 
@@ -38,9 +40,14 @@ __global__ __launch_bounds__(256) void rope_splice_kernel(
     const T *__restrict__ src_k, const T *__restrict__ src_v, T *__restrict__ ck,
     T *__restrict__ cv, const int32_t *__restrict__ map, int64_t offset, int32_t n_layers,
     int32_t n_tokens, int32_t n_heads, FastDiv div_heads, int32_t head_dim, uint32_t tpr_shift,
-    int32_t n_phys_pages, int64_t angle0, double base) {
+    int32_t n_phys_pages, int64_t angle0, double base, const RopeTab tab) {
   constexpr int N = Pack<T>::N;
   __shared__ float cs_tab[4][PER_TOKEN ? kTileTokens : 1][kMaxPairsTab];
+  // With the host's table the single-rotation instance needs 62 registers, so 8 of its
+  // workgroups would share a CU; at 8 it ran 3% slower than at the 4 its fp64 angle code allowed
+  // (config 3 shapes, 48 layers: 5.88 against 6.05 TB/s).  It reserves LDS so that 4 fit.
+  __shared__ float occ_cap[PER_TOKEN ? 1 : kOccCapFloats];
+  if (threadIdx.x >= blockDim.x) occ_cap[0] = 0.f;   // keeps the reservation
   const int j0 = blockIdx.x * kTileTokens;
   const int l = blockIdx.y;
   const int n_tok = min(kTileTokens, n_tokens - j0);
@@ -81,13 +88,19 @@ __global__ __launch_bounds__(256) void rope_splice_kernel(
 #pragma unroll
   for (int u = 0; u < kBatch; ++u) load(threadIdx.x + u * blockDim.x, cur[u]);
 
-  const int n_ang = (PER_TOKEN ? n_tok : 1) * n_pairs;
-  for (int x = threadIdx.x; x < n_ang; x += blockDim.x) {
-    const int t = x / n_pairs, i = x - t * n_pairs;
-    // PER_TOKEN: token j0 + t sits at angle0 + j0 + t; otherwise every token turns by angle0
-    const int64_t d = PER_TOKEN ? angle0 + j0 + t : angle0;
-    pair_cs(d, base, i, head_dim, cs_tab[0][t][i], cs_tab[1][t][i], cs_tab[2][t][i],
-            cs_tab[3][t][i]);
+  if constexpr (PER_TOKEN) {
+    // token j0 + t sits at angle0 + j0 + t
+    for (int x = threadIdx.x; x < n_tok * n_pairs; x += blockDim.x) {
+      const int t = x / n_pairs, i = x - t * n_pairs;
+      pair_cs(angle0 + j0 + t, base, i, head_dim, cs_tab[0][t][i], cs_tab[1][t][i],
+              cs_tab[2][t][i], cs_tab[3][t][i]);
+    }
+  } else {
+    // every token turns by angle0
+    for (int i = threadIdx.x; i < n_pairs; i += blockDim.x) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) cs_tab[q][0][i] = tab.v[q][i];
+    }
   }
   // LDS-only barrier: the item loads above stay in flight
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
@@ -153,11 +166,13 @@ hipError_t launch_rope_splice(const RopeSpliceLaunch &p, hipStream_t stream) {
   uint32_t shift = 0;
   while ((1u << shift) < tpr) ++shift;
   const FastDiv dh = make_fastdiv((uint32_t)p.n_heads);
+  RopeTab tab{};
+  if (!p.per_token) rope_tab_host(p.angle0, p.rope_base, p.head_dim, tab);
 #define NEXUS_ROPE_SPLICE(T, IL, PT)                                                              \
   hipLaunchKernelGGL((rope_splice_kernel<T, IL, PT>), grid, dim3(256), 0, stream,                \
                      (const T *)p.src_k, v_rows ? (const T *)p.src_v : nullptr, (T *)p.cache_k,  \
                      v_rows ? (T *)p.cache_v : nullptr, p.map, p.offset, p.n_layers, p.n_tokens, \
-                     p.n_heads, dh, p.head_dim, shift, p.n_phys_pages, p.angle0, p.rope_base)
+                     p.n_heads, dh, p.head_dim, shift, p.n_phys_pages, p.angle0, p.rope_base, tab)
   if (p.dtype_bytes == 2) {
     if (p.per_token) {
       if (p.interleaved) NEXUS_ROPE_SPLICE(uint16_t, true, true);
