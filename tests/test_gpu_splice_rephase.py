@@ -61,7 +61,12 @@ def test_anchored_splice_is_bit_exact():
                                                 ("bf16", N.ROPE_INTERLEAVED, 128, 1e6),
                                                 ("bf16", N.ROPE_NEOX, 256, 1e4),
                                                 ("f32", N.ROPE_NEOX, 64, 1e4),
-                                                ("f32", N.ROPE_INTERLEAVED, 64, 1e4)])
+                                                ("f32", N.ROPE_INTERLEAVED, 64, 1e4),
+                                                # head_dim > 256: the angle table is formed on
+                                                # the device instead of the host
+                                                ("bf16", N.ROPE_NEOX, 512, 1e4),
+                                                ("bf16", N.ROPE_INTERLEAVED, 1024, 1e6),
+                                                ("f32", N.ROPE_NEOX, 512, 1e4)])
 def test_rephase_block_contiguous(dtype, style, D, base):
     rng = np.random.default_rng(D + style)
     L, T, H = 3, 77, 2
