@@ -38,7 +38,7 @@ struct SeqPlan {
 struct UnitWork {
   int tgrp, split, k_begin, split_keys, n_splits;
 };
-__device__ __forceinline__ UnitWork unit_work(const SeqPlan &sp, int u) {
+__host__ __device__ __forceinline__ UnitWork unit_work(const SeqPlan &sp, int u) {
   UnitWork w;
   const int ua = sp.n_tg_a * sp.n_splits;
   int di;   // dispatch index of the task group
@@ -62,7 +62,7 @@ __device__ __forceinline__ UnitWork unit_work(const SeqPlan &sp, int u) {
   return w;
 }
 // Split count of task group `tgrp`.
-__device__ __forceinline__ int group_splits(const SeqPlan &sp, int tgrp) {
+__host__ __device__ __forceinline__ int group_splits(const SeqPlan &sp, int tgrp) {
   const int di = sp.longest_first ? sp.n_tg - 1 - tgrp : tgrp;
   return di < sp.n_tg_a ? sp.n_splits : sp.n_splits_b;
 }
@@ -97,7 +97,7 @@ struct UnitLoc {
   int seq;
   UnitWork w;
 };
-__device__ __forceinline__ UnitLoc locate_unit(const AttnPlan &plan, int unit) {
+__host__ __device__ __forceinline__ UnitLoc locate_unit(const AttnPlan &plan, int unit) {
   UnitLoc loc;
   if (!plan.range_major) {
     // sequences in dispatch order (plan.order): their first units increase along it
