@@ -1,0 +1,127 @@
+"""GPU parity of the suffix attention at the limits of its plan, against the fp64 oracle:
+
+* the most sequences one launch takes (32): all suffix-like (units taken key range by key
+  range) and mixed with causal prefills (sequence by sequence), head_dim 128 and head_dim 256
+  with a transposed V and the soft cap; every row of every sequence;
+* the longest key range one workgroup covers (32768 keys, its LDS page table full): shapes
+  whose plan gives some workgroups a single 32768-key split (the host planner test pins that
+  these plans do); sampled rows at the start, middle and end of the suffix, two KV heads;
+* a context longer than one workgroup may cover (70000 keys before 16 queries), so that every
+  row merges dozens of splits; head_dim 64 (the generic kernel), 128 and 256 with transposed V
+  and the soft cap; every row.
+
+Tolerances as the other bf16 attention tests.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2608_20397_amd import nexus as N
+from synth import PAGE
+from synth import gen as G
+
+from _pipeline import BF16_MAX_ABS, BF16_REL_RMS, compare
+
+pytestmark = pytest.mark.gpu
+
+
+def _cache(tag, n_tok, H, d, vt, k_mult=1.0, shuffle=True):
+    npp = (n_tok + PAGE - 1) // PAGE + 2
+    std = d ** -0.5
+    k = G.device_normal(2, tag, 1, (1, npp, H, PAGE, d), std * k_mult, "bf16", "cuda")
+    vshape = (1, H, d, npp * PAGE) if vt else (1, npp, H, PAGE, d)
+    v = G.device_normal(2, tag, 2, vshape, std, "bf16", "cuda")
+    perm = (np.random.default_rng([20397, 904, tag]).permutation(npp) if shuffle
+            else np.arange(npp)).astype(np.int32)
+    pm = perm[:(n_tok + PAGE - 1) // PAGE]
+    cache = N.PagedKVCache(k, v, torch.from_numpy(pm).to("cuda"), 1e4,
+                           N.V_TRANSPOSED if vt else N.V_ROWMAJOR)
+    lk, lv = O.gather_logical(G.torch_to_bits(k), G.torch_to_bits(v), pm, n_tok, PAGE,
+                              O.TRANSPOSED if vt else O.ROWMAJOR)
+    return cache, O.storage_to_f64(lk[0], "bf16"), O.storage_to_f64(lv[0], "bf16")
+
+
+def _check(got, ref, what):
+    ma, rr = compare(got, ref)
+    print(f"  {what}: max-abs {ma:.3e} rel-RMS {rr:.3e}", flush=True)
+    assert np.isfinite(got).all(), what
+    assert ma <= BF16_MAX_ABS and rr <= BF16_REL_RMS, (what, ma, rr)
+
+
+def _seqs32(r, n_tok, prefills):
+    seqs = []
+    for b in range(32):
+        if prefills and b % 5 == 2:
+            n = int(r.integers(40, 300))
+            p = int(r.integers(0, n))
+        elif b % 7 == 0:
+            n, p = 1, int(r.integers(1, n_tok))
+        else:
+            n = int(r.integers(2, 90))
+            p = int(r.integers(n, n_tok - n + 1))
+        seqs.append((n, min(p, n_tok - n)))
+    return seqs
+
+
+@pytest.mark.parametrize("d,prefills", [(128, False), (128, True), (256, False), (256, True)])
+def test_32_sequences_one_launch(d, prefills):
+    tag = 10 + d // 128 + 2 * prefills
+    vt, cap = d == 256, (50.0 if d == 256 else 0.0)
+    H, Hq, n_tok = 2, 4, 2600
+    seqs = _seqs32(np.random.default_rng([20397, 905, tag]), n_tok, prefills)
+    lens = [s[0] for s in seqs]
+    pasts = [s[1] for s in seqs]
+    starts = [int(x) for x in np.cumsum([0] + lens[:-1])]
+    print(f"32 sequences D={d} prefills={prefills}: {seqs}", flush=True)
+    cache, kk, vv = _cache(tag, n_tok, H, d, vt, 3.0 if cap else 1.0)
+    q = G.device_normal(2, tag, 0, (sum(lens), Hq, d), d ** -0.5, "bf16", "cuda")
+    out = N.suffix_attn_varlen(q, starts, lens, pasts, cache, 0, cap)
+    torch.cuda.synchronize()
+    qq = O.storage_to_f64(G.torch_to_bits(q), "bf16")
+    got = O.bf16_bits_to_f64(G.torch_to_bits(out))
+    for b, (q0, n, p) in enumerate(zip(starts, lens, pasts)):
+        ref = O.suffix_attention(qq[q0:q0 + n], kk, vv, p, softcap=cap)
+        _check(got[q0:q0 + n], ref, f"seq {b} ({n} queries at {p})")
+
+
+# (head_dim, transposed V, soft cap, H_q, H_kv, queries, n_past): plans with 32768-key splits
+LONGEST_SPLIT = [(128, False, 0.0, 40, 8, 2048, 30720), (256, True, 50.0, 16, 8, 4096, 28672)]
+
+
+@pytest.mark.parametrize("case", LONGEST_SPLIT)
+def test_longest_split_sampled(case):
+    d, vt, cap, Hq, H, n_s, n_past = case
+    g = Hq // H
+    n_tok = n_past + n_s
+    print(f"longest split: D={d} Hq={Hq} Hkv={H} {n_s} queries at {n_past}", flush=True)
+    cache, kk, vv = _cache(20 + d // 128, n_tok, H, d, vt, 3.0 if cap else 1.0)
+    q = G.device_normal(2, 20 + d // 128, 0, (n_s, Hq, d), d ** -0.5, "bf16", "cuda")
+    out = N.suffix_attn(q, cache, 0, n_past, cap)
+    torch.cuda.synchronize()
+    got = O.bf16_bits_to_f64(G.torch_to_bits(out))
+    qq = O.storage_to_f64(G.torch_to_bits(q), "bf16")
+    for kvh in (0, H - 1):
+        for r0 in (0, n_s // 2 - 2, n_s - 4):
+            rows = slice(r0, r0 + 4)
+            heads = slice(kvh * g, (kvh + 1) * g)
+            ref = O.suffix_attention(qq[rows, heads], kk[:, kvh:kvh + 1], vv[:, kvh:kvh + 1],
+                                     n_past + r0, softcap=cap)
+            _check(got[rows, heads], ref, f"kv head {kvh} rows {r0}..{r0 + 3}")
+
+
+@pytest.mark.parametrize("d,vt,cap,Hq,H", [(64, False, 0.0, 8, 2), (128, False, 0.0, 8, 2),
+                                           (256, True, 50.0, 4, 2)])
+def test_context_beyond_one_split(d, vt, cap, Hq, H):
+    n_s, n_past = 16, 70000
+    tag = 30 + d // 64
+    print(f"70000-key context: D={d} Hq={Hq} Hkv={H} vt={vt} cap={cap}", flush=True)
+    cache, kk, vv = _cache(tag, n_past + n_s, H, d, vt, 3.0 if cap else 1.0)
+    q = G.device_normal(2, tag, 0, (n_s, Hq, d), d ** -0.5, "bf16", "cuda")
+    out = N.suffix_attn(q, cache, 0, n_past, cap)
+    torch.cuda.synchronize()
+    got = O.bf16_bits_to_f64(G.torch_to_bits(out))
+    ref = O.suffix_attention(O.storage_to_f64(G.torch_to_bits(q), "bf16"), kk, vv, n_past,
+                             softcap=cap)
+    _check(got, ref, f"{n_s} queries over {n_past + n_s} keys")

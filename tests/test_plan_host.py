@@ -213,3 +213,27 @@ def test_plan_workspace_cap(harness):
     # over 32768 keys a launch must split, so the tightest caps leave some without a plan; the
     # others fall back to fewer splits (or none)
     assert 0 < n_none < len(capped)
+
+
+def test_plan_of_the_limit_launches(harness):
+    """The GPU limit tests reach what they are named for: a 32768-key split (the workgroup's
+    full page table), dozens of splits per row over a 70000-key context, and 32 sequences in
+    the range-by-range order (all suffix-like) or the sequence order (with prefills)."""
+    from test_gpu_attention_limits import LONGEST_SPLIT, _seqs32
+    longest = [(hq, hkv, d, vt, 0, [(n, p)]) for d, vt, _, hq, hkv, n, p in LONGEST_SPLIT]
+    beyond = [(8, 2, 64, False, 0, [(16, 70000)]), (8, 2, 128, False, 0, [(16, 70000)]),
+              (4, 2, 256, True, 0, [(16, 70000)])]
+    many = []
+    for d, prefills in [(128, False), (128, True), (256, False), (256, True)]:
+        tag = 10 + d // 128 + 2 * prefills
+        seqs = _seqs32(np.random.default_rng([20397, 905, tag]), 2600, prefills)
+        many.append((4, 2, d, d == 256, 0, seqs))
+    launches = longest + beyond + many
+    plans = _plans(harness, launches)
+    for launch, plan in zip(launches, plans):
+        _check(launch, plan)
+    for plan in plans[:len(longest)]:
+        assert max(x[5] for x in plan["unit"]) == MAX_SPLIT_KEYS
+    for plan in plans[len(longest):len(longest) + len(beyond)]:
+        assert min(x[6] for x in plan["unit"]) >= 30
+    assert [p["range_major"] for p in plans[-4:]] == [1, 0, 1, 0]
