@@ -125,3 +125,23 @@ def test_context_beyond_one_split(d, vt, cap, Hq, H):
     ref = O.suffix_attention(O.storage_to_f64(G.torch_to_bits(q), "bf16"), kk, vv, n_past,
                              softcap=cap)
     _check(got, ref, f"{n_s} queries over {n_past + n_s} keys")
+
+
+# Soft cap of the head_dim-256 transposed-V kernel over logit spreads (q ~ N(0, 1),
+# k ~ N(0, sd^2 / 256), so scale q.k ~ N(0, sd^2)) from barely bent by cap 50 to saturating it,
+# and caps from 8 to 2000 (the capped score is cap (1 - 2 r) with r near 1/2, so the rounding
+# of r weighs more as the cap grows).
+@pytest.mark.parametrize("sd,cap", [(3.0, 50.0), (6.0, 50.0), (10.0, 50.0), (60.0, 50.0),
+                                    (3.0, 8.0), (3.0, 300.0), (3.0, 2000.0)])
+def test_softcap_logit_spread_and_cap(sd, cap):
+    d, H, Hq, n_s, n_past = 256, 2, 4, 300, 2000
+    tag = 40 + int(sd) + int(cap) % 97
+    print(f"soft cap {cap}, logit std {sd}", flush=True)
+    cache, kk, vv = _cache(tag, n_past + n_s, H, d, True, sd)
+    q = G.device_normal(2, tag, 0, (n_s, Hq, d), 1.0, "bf16", "cuda")
+    out = N.suffix_attn(q, cache, 0, n_past, cap)
+    torch.cuda.synchronize()
+    got = O.bf16_bits_to_f64(G.torch_to_bits(out))
+    qq = O.storage_to_f64(G.torch_to_bits(q), "bf16")
+    ref = O.suffix_attention(qq, kk, vv, n_past, softcap=cap)
+    _check(got, ref, f"cap {cap} logit std {sd}")
