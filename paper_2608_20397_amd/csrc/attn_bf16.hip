@@ -522,7 +522,9 @@ bool make_plan(const AttnLaunch &p, AttnPlan &plan) {
   // at 16384).
   bool any_prefill = false;
   for (int b = 0; b < p.n_seqs; ++b) any_prefill |= p.seqs[b].n_past < p.seqs[b].len;
-  const bool range_major = p.n_seqs > 1 && !any_prefill;
+  // (beyond kMaxRanges splits of the longest length, i.e. over 2^21 keys, sequence by sequence)
+  const bool range_major = p.n_seqs > 1 && !any_prefill &&
+                           max_keys <= (int64_t)kMaxRanges * kMaxSplitKeys;
   int64_t best_sk = kMaxSplitKeys;
   double best_cost = 1e300;
   bool found = false;

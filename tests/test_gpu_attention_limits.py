@@ -145,3 +145,26 @@ def test_softcap_logit_spread_and_cap(sd, cap):
     qq = O.storage_to_f64(G.torch_to_bits(q), "bf16")
     ref = O.suffix_attention(qq, kk, vv, n_past, softcap=cap)
     _check(got, ref, f"cap {cap} logit std {sd}")
+
+
+# Two suffixes over a context of more than 2^21 keys (past the range order's 64 ranges of
+# 32768 keys: the plan takes them sequence by sequence, each row merging over 64 splits), one KV
+# head; every row.
+@pytest.mark.parametrize("d", [64, 128])
+def test_suffixes_beyond_the_range_order(d):
+    n = 64 * 32768
+    lens, pasts = [8, 8], [n + 100000, n + 50000]
+    starts = [0, 8]
+    n_tok = max(p + s for p, s in zip(pasts, lens))
+    H, Hq = 1, 4
+    tag = 60 + d // 64
+    print(f"two suffixes over {n_tok} keys, D={d}", flush=True)
+    cache, kk, vv = _cache(tag, n_tok, H, d, False)
+    q = G.device_normal(2, tag, 0, (sum(lens), Hq, d), d ** -0.5, "bf16", "cuda")
+    out = N.suffix_attn_varlen(q, starts, lens, pasts, cache, 0)
+    torch.cuda.synchronize()
+    qq = O.storage_to_f64(G.torch_to_bits(q), "bf16")
+    got = O.bf16_bits_to_f64(G.torch_to_bits(out))
+    for b, (q0, m, p) in enumerate(zip(starts, lens, pasts)):
+        ref = O.suffix_attention(qq[q0:q0 + m], kk, vv, p)
+        _check(got[q0:q0 + m], ref, f"seq {b} ({m} queries at {p})")

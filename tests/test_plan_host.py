@@ -237,3 +237,19 @@ def test_plan_of_the_limit_launches(harness):
     for plan in plans[len(longest):len(longest) + len(beyond)]:
         assert min(x[6] for x in plan["unit"]) >= 30
     assert [p["range_major"] for p in plans[-4:]] == [1, 0, 1, 0]
+
+
+def test_plan_beyond_the_range_order(harness):
+    """Suffixes over more keys than the range order's 64 ranges of 32768 keys take the sequence
+    order (each sequence with its own splits) instead of failing; at that size they keep the
+    range order."""
+    n = 64 * MAX_SPLIT_KEYS
+    launches = [(4, 1, 64, False, 0, [(8, n - 8), (8, n - 1000)]),
+                (4, 1, 64, False, 0, [(8, n + 100000), (8, n + 50000)]),
+                (8, 2, 128, False, 0, [(16, n + 20000), (1, 5000), (64, n)])]
+    plans = _plans(harness, launches)
+    for launch, plan in zip(launches, plans):
+        assert plan is not None, launch
+        _check(launch, plan)
+    assert [p["range_major"] for p in plans] == [1, 0, 0]
+    assert max(x[6] for x in plans[1]["unit"]) > 64
