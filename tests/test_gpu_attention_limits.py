@@ -8,7 +8,9 @@
   these plans do); sampled rows at the start, middle and end of the suffix, two KV heads;
 * a context longer than one workgroup may cover (70000 keys before 16 queries), so that every
   row merges dozens of splits; head_dim 64 (the generic kernel), 128 and 256 with transposed V
-  and the soft cap; every row.
+  and the soft cap; every row;
+* two suffixes over more than 2^21 keys (past the range order), and the fp32 kernel at 32
+  sequences and over a 70000-key context.
 
 Tolerances as the other bf16 attention tests.
 """
@@ -22,17 +24,17 @@ from paper_2608_20397_amd import nexus as N
 from synth import PAGE
 from synth import gen as G
 
-from _pipeline import BF16_MAX_ABS, BF16_REL_RMS, compare
+from _pipeline import BF16_MAX_ABS, BF16_REL_RMS, F32_TOL, compare
 
 pytestmark = pytest.mark.gpu
 
 
-def _cache(tag, n_tok, H, d, vt, k_mult=1.0, shuffle=True):
+def _cache(tag, n_tok, H, d, vt, k_mult=1.0, shuffle=True, dt="bf16"):
     npp = (n_tok + PAGE - 1) // PAGE + 2
     std = d ** -0.5
-    k = G.device_normal(2, tag, 1, (1, npp, H, PAGE, d), std * k_mult, "bf16", "cuda")
+    k = G.device_normal(2, tag, 1, (1, npp, H, PAGE, d), std * k_mult, dt, "cuda")
     vshape = (1, H, d, npp * PAGE) if vt else (1, npp, H, PAGE, d)
-    v = G.device_normal(2, tag, 2, vshape, std, "bf16", "cuda")
+    v = G.device_normal(2, tag, 2, vshape, std, dt, "cuda")
     perm = (np.random.default_rng([20397, 904, tag]).permutation(npp) if shuffle
             else np.arange(npp)).astype(np.int32)
     pm = perm[:(n_tok + PAGE - 1) // PAGE]
@@ -40,14 +42,17 @@ def _cache(tag, n_tok, H, d, vt, k_mult=1.0, shuffle=True):
                            N.V_TRANSPOSED if vt else N.V_ROWMAJOR)
     lk, lv = O.gather_logical(G.torch_to_bits(k), G.torch_to_bits(v), pm, n_tok, PAGE,
                               O.TRANSPOSED if vt else O.ROWMAJOR)
-    return cache, O.storage_to_f64(lk[0], "bf16"), O.storage_to_f64(lv[0], "bf16")
+    return cache, O.storage_to_f64(lk[0], dt), O.storage_to_f64(lv[0], dt)
 
 
-def _check(got, ref, what):
+def _check(got, ref, what, dt="bf16"):
     ma, rr = compare(got, ref)
     print(f"  {what}: max-abs {ma:.3e} rel-RMS {rr:.3e}", flush=True)
     assert np.isfinite(got).all(), what
-    assert ma <= BF16_MAX_ABS and rr <= BF16_REL_RMS, (what, ma, rr)
+    if dt == "bf16":
+        assert ma <= BF16_MAX_ABS and rr <= BF16_REL_RMS, (what, ma, rr)
+    else:
+        assert ma <= F32_TOL and rr <= F32_TOL, (what, ma, rr)
 
 
 def _seqs32(r, n_tok, prefills):
@@ -168,3 +173,31 @@ def test_suffixes_beyond_the_range_order(d):
     for b, (q0, m, p) in enumerate(zip(starts, lens, pasts)):
         ref = O.suffix_attention(qq[q0:q0 + m], kk, vv, p)
         _check(got[q0:q0 + m], ref, f"seq {b} ({m} queries at {p})")
+
+
+# fp32 caches (the fp32 kernel): 32 sequences in one launch (transposed V, soft cap, causal
+# prefills among them) and 16 queries over a 70000-key context; every row, fp32 tolerance.
+def test_f32_32_sequences_and_long_context():
+    H, Hq, d, n_tok = 2, 4, 64, 2600
+    seqs = _seqs32(np.random.default_rng([20397, 905, 70]), n_tok, True)
+    lens = [x[0] for x in seqs]
+    pasts = [x[1] for x in seqs]
+    starts = [int(x) for x in np.cumsum([0] + lens[:-1])]
+    print(f"f32: 32 sequences {seqs}", flush=True)
+    cache, kk, vv = _cache(70, n_tok, H, d, True, dt="f32")
+    q = G.device_normal(2, 70, 0, (sum(lens), Hq, d), d ** -0.5, "f32", "cuda")
+    out = N.suffix_attn_varlen(q, starts, lens, pasts, cache, 0, 30.0)
+    torch.cuda.synchronize()
+    qq = O.storage_to_f64(G.torch_to_bits(q), "f32")
+    got = O.storage_to_f64(G.torch_to_bits(out), "f32")
+    for b, (q0, n, p) in enumerate(zip(starts, lens, pasts)):
+        ref = O.suffix_attention(qq[q0:q0 + n], kk, vv, p, softcap=30.0)
+        _check(got[q0:q0 + n], ref, f"f32 seq {b} ({n} queries at {p})", "f32")
+    n_s, n_past, d, Hq = 16, 70000, 128, 8
+    print("f32: 16 queries over a 70000-key context", flush=True)
+    cache, kk, vv = _cache(71, n_past + n_s, H, d, False, dt="f32")
+    q = G.device_normal(2, 71, 0, (n_s, Hq, d), d ** -0.5, "f32", "cuda")
+    out = N.suffix_attn(q, cache, 0, n_past)
+    torch.cuda.synchronize()
+    ref = O.suffix_attention(O.storage_to_f64(G.torch_to_bits(q), "f32"), kk, vv, n_past)
+    _check(O.storage_to_f64(G.torch_to_bits(out), "f32"), ref, "f32 long context", "f32")
