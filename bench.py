@@ -88,6 +88,17 @@ def measured_traffic(cfg: int):
         return None
 
 
+def counters_from(cfg: int):
+    """Where `traffic` and `mfma_busy` come from: the committed counter summaries and the hash
+    of the attention sources they were taken on (which matches the sources this run built), or
+    None when they are not for these sources."""
+    files = [traffic_file(cfg), mfma_file(cfg)]
+    if any(counter_summary(f, cfg) is None for f in files):
+        return None
+    return {"files": [os.path.relpath(f, ROOT) for f in files],
+            "attention_sources_sha256": attn_sources_sha()}
+
+
 def measured_mfma_busy(cfg: int):
     """Fraction of SIMD cycles with the MFMA pipe busy in the attention kernel
     (SQ_VALU_MFMA_BUSY_CYCLES over GRBM_GUI_ACTIVE x SIMDs) from the committed counter
@@ -763,6 +774,7 @@ def config_summary(S, ms: float, mean: dict, hbm: dict, peaks: dict):
                  "mean_launch_ms": mean["attn"], "flops_per_launch": fl,
                  "traffic": measured_traffic(wl.cfg),
                  "mfma_busy": measured_mfma_busy(wl.cfg),
+                 "counters_from": counters_from(wl.cfg),
                  "alone": {"mean_launch_ms": alone_ms, "achieved_TFLOPs": tf_alone,
                            "frac": tf_alone / MFMA_BF16_PEAK_TFLOPS,
                            "timing": "the step's attention calls back to back in a HIP graph "
@@ -908,6 +920,7 @@ def main():
             "mfma_busy": measured_mfma_busy(wl.cfg),
             "mfma_busy_unit": ("fraction of SIMD cycles with the MFMA pipe busy, attention kernel "
                                "(SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs))"),
+            "counters_from": counters_from(wl.cfg),
             "algorithmic_flops_per_launch": fl_layer,
             "mean_launch_ms": mean["attn"],
             "alone": summ["attn"]["alone"],
